@@ -1,0 +1,287 @@
+/*
+ * d2sd.h - C ABI of libd2sd: the verification hot path of dual diffusion-draft
+ * speculative decoding (D^2SD, arXiv 2606.04446) on AMD Instinct MI355X (gfx950).
+ *
+ * One verify step of the target model over the confidence-guided prefix tree:
+ *
+ *   d2sd_tree_plan        host    validate (B, p_k), node counts, mask width
+ *   d2sd_tree_build       device  canonical tree arrays + ancestor-or-self masks
+ *   d2sd_cascade_verify_attention
+ *                         device  shared-prefix (context) attention, read once per
+ *                                 KV head for every tree node and GQA head, plus
+ *                                 tree-suffix attention under the ancestor mask,
+ *                                 states merged by log-sum-exp
+ *   d2sd_merge_state      device  the log-sum-exp merge of two attention states
+ *   d2sd_accept_path      device  greedy longest-accepted-path selection + bonus
+ *   d2sd_noncascade_verify_attention
+ *                         device  same attention, context re-read per tree node
+ *                                 (comparison baseline)
+ *
+ * Conventions (every entry point):
+ *  - Ownership: the caller owns every buffer. Device pointers are device memory
+ *    allocated by the caller; host pointers are ordinary host memory read only
+ *    during the call. The library never frees or retains caller memory and
+ *    allocates no device memory (the attention workspace is caller-provided).
+ *  - Streams: device entry points enqueue kernels on `stream` (0 = the null
+ *    stream) and return without synchronising. Host entry points
+ *    (d2sd_tree_plan, d2sd_cascade_workspace_size, d2sd_status_string,
+ *    d2sd_last_error) make no HIP call.
+ *  - Errors: arguments are validated on the host before any launch. On error
+ *    nothing is launched, outputs are untouched, and d2sd_last_error() returns
+ *    a thread-local message. A failed launch returns D2SD_ERR_HIP. Device
+ *    arrays whose contents disagree with the host-side sizes (node_indptr,
+ *    ctx_len, page ids) are clamped inside the kernels so that no access leaves
+ *    the buffers the host-side sizes describe; the results are then undefined.
+ *  - Layouts are row-major, innermost dimension last; no padding between rows.
+ *
+ * Notation: B is the draft block length gamma including the anchor at block
+ * position 0 (sec. 2 "DFlash", sec. 3.3 (i)); K is the number of second-draft
+ * branches (Eq. 5); branch k re-anchors at block position p_k = i_k + 1 where
+ * i_k in {0..B-2} is the selected prefix length (sec. 3.2), keeps the anchor and
+ * the first p_k - 1 first-draft tokens, and owns tree nodes for positions
+ * p_k..B-1. N_b = B + sum_k (B - p_k) is the number of tree nodes of request b.
+ */
+#ifndef D2SD_H_
+#define D2SD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status -- */
+#define D2SD_OK 0
+#define D2SD_ERR_INVALID_ARG 1          /* null pointer, bad size or value    */
+#define D2SD_ERR_UNSUPPORTED 2          /* valid but not implemented shape     */
+#define D2SD_ERR_WORKSPACE_TOO_SMALL 3  /* ws_bytes below the required size    */
+#define D2SD_ERR_HIP 4                  /* a HIP runtime call or launch failed */
+
+typedef int d2sd_status;
+
+/* Element type of q, k/v cache, k/v tree and out. Accumulation is fp32. */
+#define D2SD_F32 0
+#define D2SD_BF16 1
+
+/* Which key set d2sd_cascade_verify_attention attends to (field `stage`). */
+#define D2SD_STAGE_CASCADE 0 /* context keys + tree ancestors (the verify pass) */
+#define D2SD_STAGE_PREFIX 1  /* context keys only: the shared-prefix state      */
+#define D2SD_STAGE_TREE 2    /* tree ancestors only: the tree-suffix state      */
+
+/* Limits of this implementation. */
+#define D2SD_MAX_B 64        /* block length; a request's mask row fits 2080 nodes */
+#define D2SD_HEAD_DIM 128
+#define D2SD_PAGE_SIZE 16
+
+/* Static string for a status code; never NULL. */
+const char* d2sd_status_string(d2sd_status s);
+
+/* Detail of the last error raised on the calling thread ("" if none). The
+ * pointer stays valid until the next d2sd_* call on the same thread. */
+const char* d2sd_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int d2sd_version(void);
+
+/* ------------------------------------------------------- a1: tree build -- */
+
+/* Number of 32-bit words in one ancestor-mask row for block length B:
+ * ceil((B + B(B-1)/2) / 32), the largest node count any p set can produce
+ * (K = B-1, p = {1..B-1}). Returns 0 if B is outside [2, D2SD_MAX_B]. */
+int d2sd_mask_words(int B);
+
+/*
+ * Host. Validates the branch sets of a batch and sizes the tree (sec. 3.2,
+ * branch construction after Eq. 5; sec. 3.3 (ii)-(iii)).
+ *  batch          >= 1 requests.
+ *  B              block length, 2 <= B <= D2SD_MAX_B.
+ *  K_host[b]      branch count of request b, 0 <= K_host[b] <= min(Kmax, B-1).
+ *  p_host         [batch, Kmax]; row b holds K_host[b] distinct re-anchor
+ *                 positions in [1, B-1], any order; the rest of the row is ignored.
+ *  Kmax           row stride of p_host, >= 0.
+ *  node_indptr_host [batch+1] out: node_indptr[0] = 0,
+ *                 node_indptr[b+1] = node_indptr[b] + B + sum_k (B - p_k).
+ *  mask_words_out out (nullable): d2sd_mask_words(B).
+ * Errors: INVALID_ARG (node_indptr_host untouched).
+ */
+d2sd_status d2sd_tree_plan(int batch, int B, const int* K_host, const int* p_host, int Kmax,
+                           int* node_indptr_host, int* mask_words_out);
+
+/*
+ * Device. Builds the canonical candidate tree of every request (sec. 3.2: each
+ * branch keeps the anchor and the first p_k - 1 first-draft tokens and
+ * re-drafts positions p_k..B-1; Fig. 1(b) step 4: the K+1 candidates share
+ * their prefixes). Canonical node order of request b (indices local to b):
+ *   nodes 0..B-1        main (first-draft) chain, node j = block position j,
+ *                       parent j-1, root (the anchor) has parent -1;
+ *   then one run per branch in ascending p_k: branch k (1-based rank) owns
+ *                       B - p_k nodes for positions p_k..B-1; its first node's
+ *                       parent is main node p_k - 1, later nodes chain.
+ * Outputs (device, caller-allocated; global node index = node_indptr[b] + local):
+ *   parent[ΣN]    local parent index (-1 for the root)
+ *   depth[ΣN]     block position (0 for the root)
+ *   path_id[ΣN]   0 on the main chain, k on branch k
+ *   anc_mask[ΣN, mask_words]  ancestor-or-self set of the node over local node
+ *                 indices, bit m of the row = word m/32, bit m%32 (LSB first)
+ *   path_leaf[batch, Kmax+1]  local index of the last node of path k
+ *                 (path 0 = main chain, leaf B-1); -1 for k > K[b]
+ * Inputs: K[batch], p[batch, Kmax] (device, validated by d2sd_tree_plan; p in
+ * any order), node_indptr[batch+1] (device, from d2sd_tree_plan).
+ * total_nodes = node_indptr[batch] (host value) bounds every write.
+ * mask_words must equal d2sd_mask_words(B).
+ */
+d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int* p,
+                            const int* node_indptr, int total_nodes, int mask_words,
+                            int* parent, int* depth, int* path_id, uint32_t* anc_mask,
+                            int* path_leaf, hipStream_t stream);
+
+/* ------------------------------------------ a2-a5: cascade verify attention -- */
+
+/*
+ * Arguments of the verify attention (sec. 3.3 (iv): the target verifies the
+ * K+1 candidates in one pass with shared-prefix cascade attention; sec. 1,
+ * contribution 2: the shared context KV is reused rather than replicated per
+ * candidate). For request b, KV head h and tree node n, query head
+ * hq = h*G + g (G = num_qo_heads / num_kv_heads) attends to
+ *   context keys 0..ctx_len[b]-1 of KV head h (through the page table), and
+ *   the tree keys of the ancestors-or-self of n (bit set in anc_mask row n),
+ * with softmax scale sm_scale. Context and tree states are combined exactly
+ * by the log-sum-exp merge; the result equals one softmax over the union.
+ *
+ * Layouts (element type `dtype`):
+ *   q        [total_nodes, num_qo_heads, head_dim]   (pre-rotated queries)
+ *   k_cache, v_cache [num_pages, num_kv_heads, page_size, head_dim]
+ *   page_table [batch, max_pages] int32 physical page of logical page i
+ *   ctx_len  [batch] int32 (device), 0 <= ctx_len[b] <= max_ctx_len
+ *   k_tree, v_tree [total_nodes, num_kv_heads, head_dim] keys/values computed
+ *            for the tree nodes in this pass (the anchor is node 0)
+ *   node_indptr [batch+1] int32 (device)
+ *   anc_mask [total_nodes, mask_words] uint32 (from d2sd_tree_build)
+ *   out      [total_nodes, num_qo_heads, head_dim]
+ *   lse      [total_nodes, num_qo_heads] fp32, natural log; nullable
+ * STAGE_PREFIX writes the normalised context-only state (rows of a request
+ * with ctx_len 0 get out = 0, lse = -inf); STAGE_TREE the tree-only state.
+ */
+typedef struct d2sd_attn_args {
+  int batch;
+  int num_qo_heads;
+  int num_kv_heads;
+  int head_dim;      /* must be D2SD_HEAD_DIM */
+  int page_size;     /* must be D2SD_PAGE_SIZE */
+  int dtype;         /* D2SD_F32 or D2SD_BF16 */
+  int stage;         /* D2SD_STAGE_* */
+  float sm_scale;    /* <= 0 selects 1/sqrt(head_dim) */
+  int total_nodes;   /* host copy of node_indptr[batch] */
+  int max_nodes;     /* host upper bound of node_indptr[b+1]-node_indptr[b] */
+  int max_ctx_len;   /* host upper bound of ctx_len[b], <= max_pages*page_size */
+  int num_pages;     /* rows of k_cache / v_cache */
+  int max_pages;     /* row stride of page_table */
+  int mask_words;    /* row stride of anc_mask; >= ceil(max_nodes/32) */
+  int kv_split;      /* context tokens per split, multiple of 64; 0 = automatic */
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  const int* page_table;
+  const int* ctx_len;
+  const void* k_tree;
+  const void* v_tree;
+  const int* node_indptr;
+  const uint32_t* anc_mask;
+  void* out;
+  float* lse;
+} d2sd_attn_args;
+
+/*
+ * Host. Device workspace bytes d2sd_cascade_verify_attention needs for `args`
+ * (partial states of the context splits). Writes *bytes (0 when no split is
+ * needed). Errors: INVALID_ARG / UNSUPPORTED as the attention call would.
+ */
+d2sd_status d2sd_cascade_workspace_size(const d2sd_attn_args* args, size_t* bytes);
+
+/*
+ * Host. The context split length (tokens, multiple of 64) the attention call
+ * will use for `args` (args->kv_split if nonzero, else the automatic choice).
+ */
+d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split);
+
+/*
+ * Device. Verify attention (see d2sd_attn_args). Every context page slab of a
+ * (request, KV head) is streamed from HBM once per split and reused by all
+ * G query heads of all N_b tree nodes. ws: device workspace of ws_bytes >=
+ * d2sd_cascade_workspace_size(args) (may be NULL when that size is 0).
+ * Concurrent calls must not share a workspace.
+ */
+d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, size_t ws_bytes,
+                                          hipStream_t stream);
+
+/*
+ * Device. Log-sum-exp merge of two attention states over disjoint key sets
+ * (the cascade merge): with m = max(lse_a, lse_b), wa = exp(lse_a - m),
+ * wb = exp(lse_b - m): o = (wa*o_a + wb*o_b)/(wa+wb), lse = m + ln(wa+wb).
+ * A state with lse = -inf has weight 0; both -inf gives o = 0, lse = -inf.
+ *  o_a, o_b, o_out [rows, head_dim] fp32; lse_a, lse_b, lse_out [rows] fp32.
+ *  o_out/lse_out may alias o_a/lse_a. head_dim in [1, 1024].
+ */
+d2sd_status d2sd_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,
+                             const float* o_b, const float* lse_b, float* o_out,
+                             float* lse_out, hipStream_t stream);
+
+/*
+ * Device. The same attention as STAGE_CASCADE computed without sharing the
+ * context: one workgroup per (tree node, KV head) streams the whole context
+ * of its request, so the context is read N_b times per KV head. Comparison
+ * baseline for the cascade kernel. args->stage must be STAGE_CASCADE;
+ * kv_split is ignored. No workspace.
+ */
+d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStream_t stream);
+
+/* ----------------------------------------------------- a6: accept path -- */
+
+/*
+ * Device. Greedy longest-accepted-prefix search across the candidate tree and
+ * the bonus token (sec. 2 "DFlash": accept up to, not including, the first
+ * mismatch; sec. 3.3 (iv): commit the longest accepted prefix across branches,
+ * the target's prediction at the rejection point is the next anchor).
+ * Node c (not the root) matches iff draft_tokens[c] == target_argmax[parent(c)];
+ * c is accepted iff it and all its non-root ancestors match. L is the largest
+ * depth of an accepted node (0 if none); the chosen node is the accepted node
+ * of depth L with the lowest canonical index (main chain first, then branches
+ * by ascending p_k).
+ * Inputs (device): node_indptr[batch+1]; parent, depth[ΣN] (from
+ * d2sd_tree_build); path_id[ΣN]; draft_tokens[ΣN] (the root's entry is the
+ * anchor and is not compared); target_argmax[ΣN] (target prediction after
+ * each node).
+ * Outputs (device, caller-allocated):
+ *   accept_len[batch]   L, accepted draft tokens, 0 <= L <= B-1
+ *   best_path[batch]    path_id of the chosen node
+ *   accept_node[batch]  local index of the chosen node
+ *   path_nodes[batch, B] local nodes of depths 0..L on the chosen path, -1 after
+ *   out_tokens[batch, B] committed tokens: drafts at depths 1..L then the bonus
+ *                       target_argmax[chosen]; L+1 valid entries, -1 after
+ * total_nodes = node_indptr[batch] (host value) bounds every read.
+ */
+d2sd_status d2sd_accept_path(int batch, int B, const int* node_indptr, int total_nodes,
+                             const int* parent, const int* depth, const int* path_id,
+                             const int* draft_tokens, const int* target_argmax, int* accept_len,
+                             int* best_path, int* accept_node, int* path_nodes, int* out_tokens,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------ profiling -- */
+
+/*
+ * Host. When enabled (nonzero), d2sd_cascade_verify_attention and
+ * d2sd_noncascade_verify_attention record a HIP event pair on their stream
+ * around their main (context-streaming) kernel. d2sd_kernel_timing_collect
+ * waits for the recorded events, returns the launch count and the summed
+ * duration in milliseconds, and clears the record. Thread-safe.
+ */
+d2sd_status d2sd_kernel_timing_enable(int enable);
+d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* D2SD_H_ */
