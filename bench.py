@@ -1,0 +1,248 @@
+"""Benchmark of one verify step on one MI355X: tree build -> cascade verify
+attention -> accept path, on a seeded synthetic batch resident in HBM.
+
+    python bench.py [--steps K] [--warmup W] [--config 4] [--kv-split S]
+                    [--cpu-seconds 15] [--no-cpu-baseline] [--noncascade]
+
+Prints one JSON line. value = verified tree tokens per second of the whole
+step (tree nodes verified / step time). The roofline object describes the
+cascade attention kernel (the step's dominant kernel), timed with HIP events
+recorded by the library on its launch stream over the timed steps.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix peaks
+METRIC = "verified tree tokens/sec + prefix-KV HBM GB/s (% of peak), cascade verify attn"
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_04446_amd", "csrc", "attention.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cascade_attention_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--kv-split", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--noncascade", action="store_true", help="also time the non-cascade baseline kernel")
+    return ap.parse_args()
+
+
+def kernel_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(config: int, kv_split: int):
+    """HBM bytes per launch from committed rocprofv3 counters, if they were taken
+    on the current kernel source and the same launch configuration."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    key = f"config{config}"
+    r = rec.get(key)
+    if not r or r.get("kernel_sha") != kernel_sha() or r.get("kv_split") != kv_split:
+        return None
+    return r.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float):
+    """The oracle, as it stands, on whole requests until the time budget is spent."""
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle.attention import gather_context, request_attention
+    from oracle.tree import build_tree
+
+    done_nodes, done_req = 0, 0
+    t_total = 0.0
+    for b in range(layout.batch):
+        s, e = int(node_indptr[b]), int(node_indptr[b + 1])
+        C = int(layout.ctx_len[b])
+        npg = (C + 15) // 16
+        pages = torch.from_numpy(layout.page_table[b, :npg].astype(np.int64)).to(x["k_cache"].device)
+        kc = x["k_cache"].index_select(0, pages).float().cpu().numpy()
+        vc = x["v_cache"].index_select(0, pages).float().cpu().numpy()
+        q = x["q"][s:e].float().cpu().numpy()
+        kt = x["k_tree"][s:e].float().cpu().numpy()
+        vt = x["v_tree"][s:e].float().cpu().numpy()
+        t0 = time.perf_counter()
+        tree = build_tree(layout.spec.B, layout.p[b, :layout.K[b]])
+        kcb, vcb = gather_context(kc, vc, np.arange(npg), C, 16)
+        request_attention(q.astype(np.float64), kcb, vcb, kt.astype(np.float64), vt.astype(np.float64), tree)
+        t_total += time.perf_counter() - t0
+        done_nodes += e - s
+        done_req += 1
+        if t_total >= budget_s:
+            break
+    blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+    cores = max(blas) if blas else 1
+    return {
+        "value": done_nodes / t_total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+        "sample": f"{done_req} of {layout.batch} requests (tree build + float64 attention of every node "
+                  f"and query head over the full context and its ancestors), {t_total:.1f} s, "
+                  f"{len(os.sched_getaffinity(0))} host cores visible",
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print(f"bench.py measures one GPU only (the verify path is built and measured on a single "
+              f"MI355X); --gpus {args.gpus} / WORLD_SIZE {world} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_04446_amd import d2sd
+    from paper_2606_04446_amd import workload as wl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layout = wl.draw_layout(args.config)
+    spec = layout.spec
+    B = spec.B
+    node_indptr, W = d2sd.tree_plan(B, layout.K, layout.p)
+    total = int(node_indptr[-1])
+    max_nodes = int(np.diff(node_indptr).max())
+    max_ctx = int(layout.ctx_len.max())
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    d_K, d_p, d_ip = t(layout.K), t(layout.p), t(node_indptr)
+    d_ctx, d_pt = t(layout.ctx_len), t(layout.page_table)
+    x = wl.draw_tensors(layout, total, device=dev)
+
+    tree = d2sd.tree_build(B, d_K, d_p, d_ip, total, W)
+    torch.cuda.synchronize()
+    parent_host = tree["parent"].cpu().numpy()
+    draft, argmax = wl.draw_tokens(layout, node_indptr, parent_host)
+    d_draft, d_argmax = t(draft), t(argmax)
+    out = torch.empty_like(x["q"])
+    lse = torch.empty(x["q"].shape[:2], dtype=torch.float32, device=dev)
+    a = d2sd.attn_args(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"], d_ip,
+                       tree["anc_mask"], out, lse, total_nodes=total, max_nodes=max_nodes, max_ctx_len=max_ctx,
+                       kv_split=args.kv_split)
+    ws_bytes = d2sd.cascade_workspace_size(a)
+    kv_split = d2sd.cascade_kv_split(a)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    acc = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax)
+
+    def step():
+        d2sd.tree_build(B, d_K, d_p, d_ip, total, W, out=tree)
+        d2sd.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"],
+                                      d_ip, tree["anc_mask"], total_nodes=total, max_nodes=max_nodes,
+                                      max_ctx_len=max_ctx, kv_split=args.kv_split, out=out, lse=lse,
+                                      workspace=ws)
+        d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax,
+                         out=acc)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    d2sd.kernel_timing_collect()
+    d2sd.kernel_timing_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    d2sd.kernel_timing_enable(False)
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    launches, kern_ms_total = d2sd.kernel_timing_collect()
+    kern_ms = kern_ms_total / max(launches, 1)
+
+    # algorithmic work of one launch of the cascade kernel
+    esz = 2 if spec.dtype == "bf16" else 4
+    D, Hq, Hkv = spec.head_dim, spec.hq, spec.hkv
+    ctx = layout.ctx_len.astype(np.int64)
+    prefix_bytes = int(ctx.sum()) * Hkv * D * 2 * esz
+    depth = tree["depth"].cpu().numpy().astype(np.int64)
+    n_per_req = np.diff(node_indptr).astype(np.int64)
+    visible = np.repeat(ctx, n_per_req) + depth + 1          # keys each node attends to
+    flops = 4.0 * Hq * D * float(visible.sum())
+    t_s = kern_ms / 1e3
+    gbps = prefix_bytes / t_s / 1e9
+    tflops = flops / t_s / 1e12
+    t_hbm = prefix_bytes / (HBM_PEAK_GBPS * 1e9)
+    t_mfma = flops / (MFMA_PEAK_TFLOPS[spec.dtype] * 1e12)
+    traffic = measured_traffic(args.config, kv_split)
+    if t_mfma > t_hbm:
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_PEAK_TFLOPS[spec.dtype],
+                "unit": "TFLOP/s", "frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4), "traffic": traffic}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": traffic}
+
+    res = {
+        "metric": METRIC,
+        "value": round(total / (step_ms / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic",
+        "config": {"workload": spec.name, "batch": layout.batch,
+                   "ctx_len": [int(ctx.min()), int(ctx.max())], "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": D, "block": B, "branches": spec.K, "tree_nodes": total,
+                   "page_size": spec.page_size, "kv_split": kv_split},
+        "roofline": roof,
+        "prefix_kv_gbps": round(gbps, 1),
+        "prefix_kv_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "attn_tflops": round(tflops, 2),
+        "attn_mfma_frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4),
+        "attn_kernel_ms": round(kern_ms, 4),
+        "attn_tokens_per_s": round(total / t_s, 1),
+        "kernel_sha": kernel_sha(),
+    }
+    if args.noncascade:
+        out2 = torch.empty_like(out)
+        lse2 = torch.empty_like(lse)
+        reps = 3
+        d2sd.noncascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"],
+                                         d_ip, tree["anc_mask"], total_nodes=total, max_nodes=max_nodes,
+                                         max_ctx_len=max_ctx, out=out2, lse=lse2)
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_enable(True)
+        for _ in range(reps):
+            d2sd.noncascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"],
+                                             x["v_tree"], d_ip, tree["anc_mask"], total_nodes=total,
+                                             max_nodes=max_nodes, max_ctx_len=max_ctx, out=out2, lse=lse2)
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_enable(False)
+        n, ms = d2sd.kernel_timing_collect()
+        nc_ms = ms / max(n, 1)
+        res["noncascade"] = {"kernel_ms": round(nc_ms, 3), "speedup_of_cascade": round(nc_ms / kern_ms, 2),
+                             "requested_prefix_bytes": int((np.repeat(ctx, n_per_req)).sum()) * Hkv * D * 2 * esz,
+                             "max_abs_diff_vs_cascade": float((out2.float() - out.float()).abs().max())}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(x, layout, node_indptr, parent_host, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

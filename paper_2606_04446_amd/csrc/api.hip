@@ -1,0 +1,344 @@
+// C ABI of libd2sd: host-side validation, planning and kernel dispatch.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+d2sd_status fail(d2sd_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+d2sd_status ok() {
+  g_last_error.clear();
+  return D2SD_OK;
+}
+
+d2sd_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(D2SD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---- kernel timing (HIP events around the context-streaming kernel) ----
+std::mutex g_timing_mu;
+bool g_timing_on = false;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_timing_pending;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t take_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Reserve an event pair when timing is on (both null otherwise).
+void timing_begin(hipEvent_t* e0, hipEvent_t* e1) {
+  *e0 = *e1 = nullptr;
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  if (!g_timing_on) return;
+  *e0 = take_event();
+  *e1 = take_event();
+  if (!*e0 || !*e1) {
+    if (*e0) g_event_pool.push_back(*e0);
+    if (*e1) g_event_pool.push_back(*e1);
+    *e0 = *e1 = nullptr;
+    return;
+  }
+  g_timing_pending.emplace_back(*e0, *e1);
+}
+
+int mask_words_for(int B) {
+  if (B < 2 || B > D2SD_MAX_B) return 0;
+  return (B + B * (B - 1) / 2 + 31) / 32;
+}
+
+// ---- verify-attention planning ----
+
+constexpr int kNumCUs = 256;
+constexpr int kMinSplit = 256;
+
+d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
+  if (!a) return fail(D2SD_ERR_INVALID_ARG, "args is NULL");
+  if (a->batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", a->batch);
+  if (a->num_qo_heads < 1 || a->num_kv_heads < 1)
+    return fail(D2SD_ERR_INVALID_ARG, "head counts must be >= 1");
+  if (a->num_qo_heads % a->num_kv_heads)
+    return fail(D2SD_ERR_INVALID_ARG, "num_qo_heads %d is not a multiple of num_kv_heads %d",
+                a->num_qo_heads, a->num_kv_heads);
+  if (a->head_dim != D2SD_HEAD_DIM)
+    return fail(D2SD_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", a->head_dim, D2SD_HEAD_DIM);
+  if (a->page_size != D2SD_PAGE_SIZE)
+    return fail(D2SD_ERR_UNSUPPORTED, "page_size %d unsupported (only %d)", a->page_size, D2SD_PAGE_SIZE);
+  if (a->dtype != D2SD_F32 && a->dtype != D2SD_BF16)
+    return fail(D2SD_ERR_INVALID_ARG, "dtype %d is not D2SD_F32 or D2SD_BF16", a->dtype);
+  if (a->stage < D2SD_STAGE_CASCADE || a->stage > D2SD_STAGE_TREE)
+    return fail(D2SD_ERR_INVALID_ARG, "stage %d unknown", a->stage);
+  if (a->total_nodes < 0 || a->max_nodes < 0 || a->max_nodes > a->total_nodes)
+    return fail(D2SD_ERR_INVALID_ARG, "need 0 <= max_nodes <= total_nodes (got %d, %d)", a->max_nodes,
+                a->total_nodes);
+  if (a->total_nodes > 0 && a->max_nodes < 1)
+    return fail(D2SD_ERR_INVALID_ARG, "max_nodes must be >= 1 when total_nodes > 0");
+  if ((long long)a->total_nodes * a->num_qo_heads > (1ll << 30))
+    return fail(D2SD_ERR_UNSUPPORTED, "total_nodes * num_qo_heads exceeds 2^30 rows");
+  if (a->max_pages < 1 || a->num_pages < 1)
+    return fail(D2SD_ERR_INVALID_ARG, "max_pages and num_pages must be >= 1");
+  if (a->max_ctx_len < 0 || (long long)a->max_ctx_len > (long long)a->max_pages * a->page_size)
+    return fail(D2SD_ERR_INVALID_ARG, "max_ctx_len %d outside [0, max_pages*page_size = %lld]",
+                a->max_ctx_len, (long long)a->max_pages * a->page_size);
+  if (a->kv_split < 0 || a->kv_split % 64)
+    return fail(D2SD_ERR_INVALID_ARG, "kv_split %d must be 0 or a positive multiple of 64", a->kv_split);
+  if (a->stage != D2SD_STAGE_PREFIX && a->mask_words < (a->max_nodes + 31) / 32)
+    return fail(D2SD_ERR_INVALID_ARG, "mask_words %d too small for max_nodes %d", a->mask_words,
+                a->max_nodes);
+  if (!need_ws_fields) return D2SD_OK;
+  if (!a->q || !a->k_cache || !a->v_cache || !a->page_table || !a->ctx_len || !a->k_tree ||
+      !a->v_tree || !a->node_indptr || !a->out)
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  if (a->stage != D2SD_STAGE_PREFIX && !a->anc_mask)
+    return fail(D2SD_ERR_INVALID_ARG, "anc_mask is NULL");
+  return D2SD_OK;
+}
+
+// Context tokens per split. Automatic choice: enough (request, KV head, row
+// group, split) work items for about two workgroups per CU, but no split
+// shorter than kMinSplit tokens (the partial state of a split costs as many
+// bytes as ~M/2 keys of K/V, M = rows sharing it).
+int choose_split(const d2sd_attn_args* a, int G) {
+  if (a->kv_split > 0) return a->kv_split;
+  const int ctx = a->max_ctx_len;
+  if (ctx <= kMinSplit) return ((max(ctx, 1) + 63) / 64) * 64;
+  const double avg_nodes = (double)a->total_nodes / a->batch;
+  const int avg_tiles = (int)ceil(avg_nodes * G / d2sd::kRowsPerTile);
+  const int tiles_per_group = d2sd::group_rows(a->dtype) / d2sd::kRowsPerTile;
+  const int avg_groups = max(1, (avg_tiles + tiles_per_group - 1) / tiles_per_group);
+  const long long base = (long long)a->batch * a->num_kv_heads * avg_groups;
+  int splits = (int)((2ll * kNumCUs + base - 1) / base);
+  splits = max(1, min(splits, ctx / kMinSplit));
+  const int per = (ctx + splits - 1) / splits;
+  return ((per + 63) / 64) * 64;
+}
+
+d2sd_status make_plan(const d2sd_attn_args* a, d2sd::AttnPlan* plan) {
+  plan->G = a->num_qo_heads / a->num_kv_heads;
+  plan->split = choose_split(a, plan->G);
+  const bool ctx = a->stage != D2SD_STAGE_TREE;
+  plan->n_ch_max = ctx ? max(1, (a->max_ctx_len + plan->split - 1) / plan->split) : 1;
+  const long long max_rows = (long long)a->max_nodes * plan->G;
+  const int rows_per_group = d2sd::group_rows(a->dtype);
+  plan->n_rg_max = (int)max(1ll, (max_rows + rows_per_group - 1) / rows_per_group);
+  plan->items = (long long)a->batch * a->num_kv_heads * plan->n_ch_max * plan->n_rg_max;
+  if (plan->items > (1ll << 30)) return fail(D2SD_ERR_UNSUPPORTED, "too many work items (%lld)", plan->items);
+  const size_t rows = (size_t)a->total_nodes * a->num_qo_heads;
+  plan->ws_bytes = plan->n_ch_max > 1 ? (size_t)plan->n_ch_max * rows * (a->head_dim + 2) * sizeof(float) : 0;
+  plan->scale = a->sm_scale > 0.0f ? a->sm_scale : 1.0f / sqrtf((float)a->head_dim);
+  return D2SD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* d2sd_status_string(d2sd_status s) {
+  switch (s) {
+    case D2SD_OK: return "ok";
+    case D2SD_ERR_INVALID_ARG: return "invalid argument";
+    case D2SD_ERR_UNSUPPORTED: return "unsupported";
+    case D2SD_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case D2SD_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* d2sd_last_error(void) { return g_last_error.c_str(); }
+
+int d2sd_version(void) { return 100; }
+
+int d2sd_mask_words(int B) { return mask_words_for(B); }
+
+d2sd_status d2sd_tree_plan(int batch, int B, const int* K_host, const int* p_host, int Kmax,
+                           int* node_indptr_host, int* mask_words_out) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (B < 2 || B > D2SD_MAX_B) return fail(D2SD_ERR_INVALID_ARG, "B = %d outside [2, %d]", B, D2SD_MAX_B);
+  if (Kmax < 0) return fail(D2SD_ERR_INVALID_ARG, "Kmax must be >= 0");
+  if (!K_host || !node_indptr_host || (Kmax > 0 && !p_host))
+    return fail(D2SD_ERR_INVALID_ARG, "a required host pointer is NULL");
+  std::vector<int> indptr(batch + 1, 0);
+  for (int b = 0; b < batch; ++b) {
+    const int K = K_host[b];
+    if (K < 0 || K > Kmax || K > B - 1)
+      return fail(D2SD_ERR_INVALID_ARG, "request %d: K = %d outside [0, min(Kmax=%d, B-1=%d)]", b, K, Kmax,
+                  B - 1);
+    unsigned long long seen = 0ull;
+    long long n = B;
+    for (int k = 0; k < K; ++k) {
+      const int pk = p_host[(size_t)b * Kmax + k];
+      if (pk < 1 || pk > B - 1)
+        return fail(D2SD_ERR_INVALID_ARG, "request %d: re-anchor position %d outside [1, %d]", b, pk, B - 1);
+      if ((seen >> pk) & 1ull)
+        return fail(D2SD_ERR_INVALID_ARG, "request %d: re-anchor position %d repeated", b, pk);
+      seen |= 1ull << pk;
+      n += B - pk;
+    }
+    if ((long long)indptr[b] + n > (1ll << 30)) return fail(D2SD_ERR_INVALID_ARG, "too many tree nodes");
+    indptr[b + 1] = indptr[b] + (int)n;
+  }
+  for (int b = 0; b <= batch; ++b) node_indptr_host[b] = indptr[b];
+  if (mask_words_out) *mask_words_out = mask_words_for(B);
+  return ok();
+}
+
+d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int* p,
+                            const int* node_indptr, int total_nodes, int mask_words, int* parent,
+                            int* depth, int* path_id, uint32_t* anc_mask, int* path_leaf,
+                            hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (B < 2 || B > D2SD_MAX_B) return fail(D2SD_ERR_INVALID_ARG, "B = %d outside [2, %d]", B, D2SD_MAX_B);
+  if (Kmax < 0) return fail(D2SD_ERR_INVALID_ARG, "Kmax must be >= 0");
+  if (total_nodes < 0) return fail(D2SD_ERR_INVALID_ARG, "total_nodes must be >= 0");
+  if (mask_words != mask_words_for(B))
+    return fail(D2SD_ERR_INVALID_ARG, "mask_words %d != d2sd_mask_words(%d) = %d", mask_words, B,
+                mask_words_for(B));
+  if (!K || (Kmax > 0 && !p) || !node_indptr || !parent || !depth || !path_id || !anc_mask || !path_leaf)
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  return hip_status(d2sd::launch_tree_build(batch, B, Kmax, K, p, node_indptr, total_nodes, mask_words,
+                                            parent, depth, path_id, anc_mask, path_leaf, stream),
+                    "tree_build launch");
+}
+
+d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split) {
+  d2sd_status s = validate_attn(args, false);
+  if (s) return s;
+  if (!kv_split) return fail(D2SD_ERR_INVALID_ARG, "kv_split is NULL");
+  d2sd::AttnPlan plan;
+  if ((s = make_plan(args, &plan))) return s;
+  *kv_split = plan.split;
+  return ok();
+}
+
+d2sd_status d2sd_cascade_workspace_size(const d2sd_attn_args* args, size_t* bytes) {
+  d2sd_status s = validate_attn(args, false);
+  if (s) return s;
+  if (!bytes) return fail(D2SD_ERR_INVALID_ARG, "bytes is NULL");
+  d2sd::AttnPlan plan;
+  if ((s = make_plan(args, &plan))) return s;
+  *bytes = plan.ws_bytes;
+  return ok();
+}
+
+d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, size_t ws_bytes,
+                                          hipStream_t stream) {
+  d2sd_status s = validate_attn(args, true);
+  if (s) return s;
+  d2sd::AttnPlan plan;
+  if ((s = make_plan(args, &plan))) return s;
+  if (plan.ws_bytes > 0 && (!ws || ws_bytes < plan.ws_bytes))
+    return fail(D2SD_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws ? ws_bytes : 0,
+                plan.ws_bytes);
+  if (args->total_nodes == 0) return ok();
+  hipEvent_t e0, e1;
+  timing_begin(&e0, &e1);
+  return hip_status(d2sd::launch_cascade_attention(*args, plan, ws, stream, e0, e1),
+                    "cascade attention launch");
+}
+
+d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStream_t stream) {
+  d2sd_status s = validate_attn(args, true);
+  if (s) return s;
+  if (args->stage != D2SD_STAGE_CASCADE)
+    return fail(D2SD_ERR_INVALID_ARG, "the non-cascade baseline computes STAGE_CASCADE only");
+  if ((long long)args->batch * args->num_kv_heads * args->max_nodes > (1ll << 30))
+    return fail(D2SD_ERR_UNSUPPORTED, "too many work items");
+  if (args->num_qo_heads / args->num_kv_heads > d2sd::group_rows(args->dtype))
+    return fail(D2SD_ERR_UNSUPPORTED, "the baseline supports at most %d query heads per KV head",
+                d2sd::group_rows(args->dtype));
+  if (args->total_nodes == 0) return ok();
+  const float scale = args->sm_scale > 0.0f ? args->sm_scale : 1.0f / sqrtf((float)args->head_dim);
+  hipEvent_t e0, e1;
+  timing_begin(&e0, &e1);
+  return hip_status(d2sd::launch_noncascade_attention(*args, scale, stream, e0, e1),
+                    "non-cascade attention launch");
+}
+
+d2sd_status d2sd_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,
+                             const float* o_b, const float* lse_b, float* o_out, float* lse_out,
+                             hipStream_t stream) {
+  if (rows < 0) return fail(D2SD_ERR_INVALID_ARG, "rows must be >= 0");
+  if (head_dim < 1 || head_dim > 1024) return fail(D2SD_ERR_INVALID_ARG, "head_dim %d outside [1, 1024]", head_dim);
+  if (!o_a || !lse_a || !o_b || !lse_b || !o_out || !lse_out)
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  if (rows == 0) return ok();
+  return hip_status(d2sd::launch_merge_state(rows, head_dim, o_a, lse_a, o_b, lse_b, o_out, lse_out, stream),
+                    "merge_state launch");
+}
+
+d2sd_status d2sd_accept_path(int batch, int B, const int* node_indptr, int total_nodes,
+                             const int* parent, const int* depth, const int* path_id,
+                             const int* draft_tokens, const int* target_argmax, int* accept_len,
+                             int* best_path, int* accept_node, int* path_nodes, int* out_tokens,
+                             hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (B < 2 || B > D2SD_MAX_B) return fail(D2SD_ERR_INVALID_ARG, "B = %d outside [2, %d]", B, D2SD_MAX_B);
+  if (total_nodes < 0) return fail(D2SD_ERR_INVALID_ARG, "total_nodes must be >= 0");
+  if (!node_indptr || !parent || !depth || !path_id || !draft_tokens || !target_argmax || !accept_len ||
+      !best_path || !accept_node || !path_nodes || !out_tokens)
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  return hip_status(d2sd::launch_accept_path(batch, B, node_indptr, total_nodes, parent, depth, path_id,
+                                             draft_tokens, target_argmax, accept_len, best_path,
+                                             accept_node, path_nodes, out_tokens, stream),
+                    "accept_path launch");
+}
+
+d2sd_status d2sd_kernel_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  g_timing_on = enable != 0;
+  return ok();
+}
+
+d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms) {
+  if (!launches || !total_ms) return fail(D2SD_ERR_INVALID_ARG, "output pointer is NULL");
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pend;
+  {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    pend.swap(g_timing_pending);
+  }
+  double sum = 0.0;
+  hipError_t err = hipSuccess;
+  for (auto& pr : pend) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(pr.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+    sum += ms;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    for (auto& pr : pend) {
+      g_event_pool.push_back(pr.first);
+      g_event_pool.push_back(pr.second);
+    }
+  }
+  *launches = (int)pend.size();
+  *total_ms = sum;
+  return hip_status(err, "kernel timing");
+}
+
+}  // extern "C"

@@ -1,0 +1,668 @@
+// Cascade verify attention over the candidate tree (sec. 3.3 (iv): the K+1
+// candidates are verified in one target pass with shared-prefix cascade
+// attention; sec. 1, contribution 2: the shared context is reused instead of
+// being replicated per candidate).
+//
+// Work decomposition. For one request b and KV head h, the M = N_b * G query
+// rows (tree node n, query head h*G+g, row index n*G+g) all attend to the same
+// context keys, so they are stacked into the column dimension of one dense
+// contraction. A workgroup (4 waves, one per SIMD) owns up to 8 column tiles
+// of 32 rows and one split of the context; every 64-key K/V tile of that
+// split is fetched from HBM once (128-bit coalesced loads of whole 4 KB page
+// slabs), staged in LDS and consumed by all its rows. The tree keys of the
+// request are appended to split 0 under the ancestor mask, so the tree state
+// joins the context state through the same online log-sum-exp rescale.
+//
+// Per tile and wave: S^T = K Q^T with MFMA (keys on the MFMA row axis,
+// queries on the column axis), so a lane owns one query and 16 keys of each
+// 32-key block; the row max needs one cross-half exchange and the row sum
+// stays lane-local. P^T leaves the accumulator already in MFMA B-operand
+// order; V is written to LDS transposed with the matching key permutation, so
+// O^T += V^T P^T needs no register shuffles. Split partials (unnormalised O,
+// running max in log2 units, running sum) go to the workspace and a second
+// kernel merges them by log-sum-exp; a request with a single split is
+// finalised in place.
+#include <math.h>
+
+#include "common.h"
+
+namespace d2sd {
+
+namespace {
+
+constexpr int kD = 128;
+constexpr int kThreads = 256;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+struct Params {
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  const int* page_table;
+  const int* ctx_len;
+  const void* k_tree;
+  const void* v_tree;
+  const int* node_indptr;
+  const uint32_t* anc_mask;
+  void* out;
+  float* lse;
+  float* ws_o;  // [n_ch_max, total_rows, D]
+  float* ws_m;  // [n_ch_max, total_rows]
+  float* ws_l;  // [n_ch_max, total_rows]
+  int batch, hq, hkv, G, stage;
+  int total_nodes, max_nodes, max_ctx, num_pages, max_pages, mask_words;
+  int split, n_ch_max, n_rg_max, items;
+  int node_mode;  // 1: one workgroup per (request, node, KV head), no context sharing
+  float c2;  // sm_scale * log2(e)
+};
+
+// Element-type specific tiling.
+template <typename T>
+struct Tile;
+
+template <>
+struct Tile<__bf16> {
+  static constexpr int KT = 64;         // keys per tile
+  static constexpr int WT = 2;          // 32-query column tiles per wave
+  static constexpr int KS = 136;        // K row stride (elements): 272 B, conflict-free b128 reads
+  static constexpr int VS = 72;         // V^T row stride (elements): 144 B
+  static constexpr int K_ELEMS = KT * KS;
+  static constexpr int V_ELEMS = kD * VS;
+};
+
+template <>
+struct Tile<float> {
+  static constexpr int KT = 32;
+  static constexpr int WT = 1;
+  static constexpr int KS = 130;        // K row stride (floats)
+  static constexpr int VS = 136;        // V row stride (floats), V kept key-major
+  static constexpr int K_ELEMS = KT * KS;
+  static constexpr int V_ELEMS = KT * VS;
+};
+
+__device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma(float a, float b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
+
+// Pointer to the first element of key `kabs` of request b / KV head h, or null
+// when the key lies outside [0, key_end). Context keys go through the page
+// table, tree keys index the tree K/V rows of the request.
+template <typename T>
+__device__ __forceinline__ const T* key_row(const Params& p, const T* base_cache, const T* base_tree,
+                                            bool tree, int b, int h, int node_base, int kabs,
+                                            int key_end) {
+  if (kabs >= key_end) return nullptr;
+  if (tree) return base_tree + ((size_t)(node_base + kabs) * p.hkv + h) * kD;
+  int page = p.page_table[(size_t)b * p.max_pages + (kabs >> 4)];
+  page = clampi(page, 0, p.num_pages - 1);
+  return base_cache + (((size_t)page * p.hkv + h) * D2SD_PAGE_SIZE + (kabs & 15)) * kD;
+}
+
+// ---- staging of one K/V tile: global -> registers -> LDS ------------------
+
+struct StageBf16 {
+  uint4 k[4];
+  uint4 v[4];
+};
+
+// bf16: K chunk i of thread t covers key 16i + t/16, dims (t%16)*8..+8, so the
+// 256 threads read one 4 KB page slab per i. V: thread t covers dims
+// (t/16)*8..+8 of the 4 keys 4*(t%16)..+3 (transposed when stored).
+__device__ __forceinline__ void load_tile(const Params& p, StageBf16& st, bool tree, int b, int h,
+                                          int node_base, int key0, int key_end) {
+  const __bf16* kc = static_cast<const __bf16*>(p.k_cache);
+  const __bf16* vc = static_cast<const __bf16*>(p.v_cache);
+  const __bf16* kt = static_cast<const __bf16*>(p.k_tree);
+  const __bf16* vt = static_cast<const __bf16*>(p.v_tree);
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int key = 16 * i + (t >> 4);
+    const __bf16* r = key_row(p, kc, kt, tree, b, h, node_base, key0 + key, key_end);
+    st.k[i] = r ? *reinterpret_cast<const uint4*>(r + (t & 15) * 8) : zero4();
+  }
+  const int oct = t >> 4;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int key = 4 * (t & 15) + e;
+    const __bf16* r = key_row(p, vc, vt, tree, b, h, node_base, key0 + key, key_end);
+    st.v[e] = r ? *reinterpret_cast<const uint4*>(r + oct * 8) : zero4();
+  }
+}
+
+__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
+__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
+
+__device__ __forceinline__ void store_tile(const StageBf16& st, __bf16* sK, __bf16* sV) {
+  using C = Tile<__bf16>;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int key = 16 * i + (t >> 4);
+    *reinterpret_cast<uint4*>(sK + key * C::KS + (t & 15) * 8) = st.k[i];
+  }
+  // V^T: the 4 keys of this thread land in 4 adjacent columns of the permuted
+  // key order (within each 16-key group: 0-3, 8-11 | 4-7, 12-15), which is the
+  // order the PV B operand takes straight from the S^T accumulator.
+  const int kq = t & 15;
+  const int col = (kq >> 2) * 16 + (kq & 1) * 8 + ((kq >> 1) & 1) * 4;
+  const int dim0 = (t >> 4) * 8;
+  const uint32_t w0[4] = {st.v[0].x, st.v[0].y, st.v[0].z, st.v[0].w};
+  const uint32_t w1[4] = {st.v[1].x, st.v[1].y, st.v[1].z, st.v[1].w};
+  const uint32_t w2[4] = {st.v[2].x, st.v[2].y, st.v[2].z, st.v[2].w};
+  const uint32_t w3[4] = {st.v[3].x, st.v[3].y, st.v[3].z, st.v[3].w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint2 even = make_uint2(lo_pair(w0[j], w1[j]), lo_pair(w2[j], w3[j]));
+    uint2 odd = make_uint2(hi_pair(w0[j], w1[j]), hi_pair(w2[j], w3[j]));
+    *reinterpret_cast<uint2*>(sV + (dim0 + 2 * j) * C::VS + col) = even;
+    *reinterpret_cast<uint2*>(sV + (dim0 + 2 * j + 1) * C::VS + col) = odd;
+  }
+}
+
+struct StageF32 {
+  uint4 k[4];
+  uint4 v[4];
+};
+
+// fp32: 32 keys x 128 dims per tile; chunk c = t + 256 i covers key c/32,
+// dims (c%32)*4..+4, for K and V alike (V stays key-major).
+__device__ __forceinline__ void load_tile(const Params& p, StageF32& st, bool tree, int b, int h,
+                                          int node_base, int key0, int key_end) {
+  const float* kc = static_cast<const float*>(p.k_cache);
+  const float* vc = static_cast<const float*>(p.v_cache);
+  const float* kt = static_cast<const float*>(p.k_tree);
+  const float* vt = static_cast<const float*>(p.v_tree);
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int key = 8 * i + (t >> 5);
+    const int d4 = (t & 31) * 4;
+    const float* rk = key_row(p, kc, kt, tree, b, h, node_base, key0 + key, key_end);
+    const float* rv = key_row(p, vc, vt, tree, b, h, node_base, key0 + key, key_end);
+    st.k[i] = rk ? *reinterpret_cast<const uint4*>(rk + d4) : zero4();
+    st.v[i] = rv ? *reinterpret_cast<const uint4*>(rv + d4) : zero4();
+  }
+}
+
+__device__ __forceinline__ void store_tile(const StageF32& st, float* sK, float* sV) {
+  using C = Tile<float>;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int key = 8 * i + (t >> 5);
+    const int d4 = (t & 31) * 4;
+    *reinterpret_cast<uint2*>(sK + key * C::KS + d4) = make_uint2(st.k[i].x, st.k[i].y);
+    *reinterpret_cast<uint2*>(sK + key * C::KS + d4 + 2) = make_uint2(st.k[i].z, st.k[i].w);
+    *reinterpret_cast<uint4*>(sV + key * C::VS + d4) = st.v[i];
+  }
+}
+
+template <typename T>
+struct Frag;
+template <>
+struct Frag<__bf16> {
+  using Q = bf16x8;
+  static constexpr int QN = 8;   // k-steps over the head dim (16 dims each)
+};
+template <>
+struct Frag<float> {
+  using Q = float;
+  static constexpr int QN = 64;  // k-steps over the head dim (2 dims each)
+};
+
+// Head-dim assignment of the S^T = K Q^T k-steps (must agree for K and Q).
+// bf16: step s, lane half hf holds dims hf*64 + s*8 .. +8.
+// fp32: step s, lane half hf holds dim 2s + hf.
+__device__ __forceinline__ void load_q(const Params& p, bf16x8 (&qf)[8], const __bf16* row, int hf) {
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    if (row) {
+      uint4 u = *reinterpret_cast<const uint4*>(row + hf * 64 + s * 8);
+      qf[s] = __builtin_bit_cast(bf16x8, u);
+    } else {
+      qf[s] = __builtin_bit_cast(bf16x8, zero4());
+    }
+  }
+}
+__device__ __forceinline__ void load_q(const Params& p, float (&qf)[64], const float* row, int hf) {
+#pragma unroll
+  for (int s = 0; s < 64; ++s) qf[s] = row ? row[2 * s + hf] : 0.0f;
+}
+
+// S^T block (32 keys starting at key row kb of the LDS tile) for one query tile.
+__device__ __forceinline__ f32x16 score_block(const __bf16* sK, int kb, const bf16x8 (&qf)[8],
+                                              int lane) {
+  using C = Tile<__bf16>;
+  f32x16 acc = {};
+  const int hf = lane >> 5;
+  const __bf16* base = sK + (kb + (lane & 31)) * C::KS + hf * 64;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + s * 8));
+    acc = mfma(a, qf[s], acc);
+  }
+  return acc;
+}
+__device__ __forceinline__ f32x16 score_block(const float* sK, int kb, const float (&qf)[64],
+                                              int lane) {
+  using C = Tile<float>;
+  f32x16 acc = {};
+  const int hf = lane >> 5;
+  const float* base = sK + (kb + (lane & 31)) * C::KS + hf;
+#pragma unroll
+  for (int s = 0; s < 64; ++s) acc = mfma(base[2 * s], qf[s], acc);
+  return acc;
+}
+
+// O^T (4 dim tiles of 32) += V^T P^T for one 32-key block of the tile.
+// bf16: the block's probabilities p[0..15] become two 16-key k-steps.
+__device__ __forceinline__ void pv_block(const __bf16* sV, int kb, const f32x16& pr,
+                                         f32x16 (&o)[4], int lane) {
+  using C = Tile<__bf16>;
+  const int hf = lane >> 5;
+  bf16x8 b0, b1;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    b0[j] = (__bf16)pr[j];
+    b1[j] = (__bf16)pr[8 + j];
+  }
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    const __bf16* base = sV + (dt * 32 + (lane & 31)) * C::VS + kb + hf * 8;
+    bf16x8 a0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base));
+    bf16x8 a1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + 16));
+    o[dt] = mfma(a0, b0, o[dt]);
+    o[dt] = mfma(a1, b1, o[dt]);
+  }
+}
+// fp32: accumulator slot i of lane half hf is key kb + (i/4)*8 + hf*4 + i%4.
+__device__ __forceinline__ void pv_block(const float* sV, int kb, const f32x16& pr, f32x16 (&o)[4],
+                                         int lane) {
+  using C = Tile<float>;
+  const int hf = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int key = kb + (i >> 2) * 8 + hf * 4 + (i & 3);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) o[dt] = mfma(sV[key * C::VS + dt * 32 + (lane & 31)], pr[i], o[dt]);
+  }
+}
+
+template <typename T>
+struct Stage;
+template <>
+struct Stage<__bf16> {
+  using type = StageBf16;
+};
+template <>
+struct Stage<float> {
+  using type = StageF32;
+};
+
+template <typename T>
+__device__ __forceinline__ void store_out(T* dst, const float* v4);
+template <>
+__device__ __forceinline__ void store_out<__bf16>(__bf16* dst, const float* v) {
+  __bf16 h[4] = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+  *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(h);
+}
+template <>
+__device__ __forceinline__ void store_out<float>(float* dst, const float* v) {
+  *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
+  using C = Tile<T>;
+  using QF = typename Frag<T>::Q;
+  constexpr int KT = C::KT;
+  constexpr int QN = Frag<T>::QN;
+  constexpr int NBLK = KT / 32;   // 32-key blocks per tile
+  constexpr int WT = C::WT;
+  constexpr int GROUP_ROWS = 4 * WT * kRowsPerTile;
+
+  __shared__ __attribute__((aligned(16))) T smem[2 * (C::K_ELEMS + C::V_ELEMS)];
+
+  // ---- work item (XCD-aware: consecutive items share an XCD and its L2) ----
+  const int per_xcd = gridDim.x / 8;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= p.items) return;
+  int rest = item;
+  int rg = 0, ch = 0, n_sel = 0;
+  if (p.node_mode) {
+    n_sel = rest % p.max_nodes; rest /= p.max_nodes;
+  } else {
+    rg = rest % p.n_rg_max; rest /= p.n_rg_max;
+    ch = rest % p.n_ch_max; rest /= p.n_ch_max;
+  }
+  const int h = rest % p.hkv;
+  const int b = rest / p.hkv;
+
+  const int node_base = clampi(p.node_indptr[b], 0, p.total_nodes);
+  const int Nb = clampi(p.node_indptr[b + 1] - node_base, 0, min(p.max_nodes, p.total_nodes - node_base));
+  const int Mb = Nb * p.G;
+  // rows [r_lo, r_hi) of the (request, KV head) column block owned by this workgroup
+  int r_lo, r_hi;
+  if (p.node_mode) {
+    if (n_sel >= Nb) return;
+    r_lo = n_sel * p.G;
+    r_hi = r_lo + p.G;
+  } else {
+    r_lo = rg * GROUP_ROWS;
+    if (r_lo >= Mb) return;
+    r_hi = min(Mb, r_lo + GROUP_ROWS);
+  }
+  const int Cb = clampi(p.ctx_len[b], 0, p.max_ctx);
+  const bool use_ctx = p.stage != D2SD_STAGE_TREE;
+  const bool use_tree = p.stage != D2SD_STAGE_PREFIX;
+  const int n_ch_b = use_ctx ? max(1, ceil_div(Cb, p.split)) : 1;
+  if (ch >= n_ch_b) return;
+  const int c0 = use_ctx ? ch * p.split : 0;
+  const int c1 = use_ctx ? min(Cb, c0 + p.split) : 0;
+  const int n_ctx_tiles = c1 > c0 ? ceil_div(c1 - c0, KT) : 0;
+  const int n_tree_tiles = (use_tree && ch == 0) ? ceil_div(Nb, KT) : 0;
+  const int n_tiles = n_ctx_tiles + n_tree_tiles;
+
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int hf = lane >> 5;
+  const int tiles_wg = ceil_div(r_hi - r_lo, kRowsPerTile);
+  // query tiles of this wave: wave and wave + 4 (balanced over the 4 SIMDs)
+  const int nq = min(WT, (wave < tiles_wg) + (wave + 4 < tiles_wg));
+
+  QF qf[WT][QN];
+  int qnode[WT];
+  int qrow[WT];  // global output row (node * hq + head) or -1
+#pragma unroll
+  for (int j = 0; j < WT; ++j) {
+    const int r = r_lo + (wave + 4 * j) * kRowsPerTile + (lane & 31);
+    const bool valid = j < nq && r < r_hi;
+    const int n = valid ? r / p.G : 0;
+    const int g = valid ? r % p.G : 0;
+    qnode[j] = n;
+    qrow[j] = valid ? (node_base + n) * p.hq + h * p.G + g : -1;
+    const T* row = valid ? static_cast<const T*>(p.q) + (size_t)qrow[j] * kD : nullptr;
+    load_q(p, qf[j], row, hf);
+  }
+
+  f32x16 o[WT][4];
+  float m_run[WT], l_run[WT];
+#pragma unroll
+  for (int j = 0; j < WT; ++j) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) o[j][dt] = f32x16{};
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.0f;
+  }
+
+  // two LDS stages, each [K tile | V tile]
+  auto stage_k = [&](int i) { return smem + i * (C::K_ELEMS + C::V_ELEMS); };
+  auto stage_v = [&](int i) { return smem + i * (C::K_ELEMS + C::V_ELEMS) + C::K_ELEMS; };
+  typename Stage<T>::type st;
+
+  auto tile_src = [&](int j, bool& tree, int& key0, int& key_end) {
+    tree = j >= n_ctx_tiles;
+    key0 = tree ? (j - n_ctx_tiles) * KT : c0 + j * KT;
+    key_end = tree ? Nb : c1;
+  };
+
+  if (n_tiles > 0) {
+    bool tr; int k0, ke;
+    tile_src(0, tr, k0, ke);
+    load_tile(p, st, tr, b, h, node_base, k0, ke);
+    store_tile(st, stage_k(0), stage_v(0));
+  }
+  __syncthreads();
+
+  for (int jt = 0; jt < n_tiles; ++jt) {
+    const int cur = jt & 1;
+    if (jt + 1 < n_tiles) {
+      bool tr; int k0, ke;
+      tile_src(jt + 1, tr, k0, ke);
+      load_tile(p, st, tr, b, h, node_base, k0, ke);
+    }
+    bool is_tree; int key0, key_end;
+    tile_src(jt, is_tree, key0, key_end);
+#pragma unroll
+    for (int j = 0; j < WT; ++j) {
+      if (j >= nq) break;
+      // scores of this tile: NBLK blocks of 32 keys, slot i of block kb is key
+      // key0 + 32 kb + (i/4)*8 + hf*4 + i%4
+      f32x16 s[NBLK];
+#pragma unroll
+      for (int kb = 0; kb < NBLK; ++kb) s[kb] = score_block(stage_k(cur), 32 * kb, qf[j], lane);
+      uint64_t vis = ~0ull;  // visible-key bits of this tile for the lane's node
+      if (is_tree) {
+        const uint32_t* mrow = p.anc_mask + (size_t)(node_base + qnode[j]) * p.mask_words;
+        const int w0 = key0 >> 5;
+        const uint32_t lo = w0 < p.mask_words ? mrow[w0] : 0u;
+        const uint32_t hi = (KT > 32 && w0 + 1 < p.mask_words) ? mrow[w0 + 1] : 0u;
+        vis = (uint64_t)lo | ((uint64_t)hi << 32);
+      }
+      const int nvalid = key_end - key0;  // keys >= nvalid are padding
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < NBLK; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int k = 32 * kb + (i >> 2) * 8 + hf * 4 + (i & 3);
+          const bool ok = k < nvalid && ((vis >> k) & 1ull);
+          s[kb][i] = ok ? s[kb][i] : -INFINITY;
+          mx = fmaxf(mx, s[kb][i]);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run[j], mx);
+      const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_use) * p.c2);
+      const float moff = m_use * p.c2;
+      float lsum = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < NBLK; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][i], p.c2, -moff));
+          s[kb][i] = e;
+          lsum += e;
+        }
+      }
+      l_run[j] = l_run[j] * alpha + lsum;
+      m_run[j] = m_new;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) o[j][dt] *= alpha;
+#pragma unroll
+      for (int kb = 0; kb < NBLK; ++kb) pv_block(stage_v(cur), 32 * kb, s[kb], o[j], lane);
+    }
+    if (jt + 1 < n_tiles) store_tile(st, stage_k(cur ^ 1), stage_v(cur ^ 1));
+    __syncthreads();
+  }
+
+  // ---- epilogue: finalise (single split) or write the split partial ----
+  const bool direct = n_ch_b == 1;
+#pragma unroll
+  for (int j = 0; j < WT; ++j) {
+    if (j >= nq) break;
+    const float l_all = l_run[j] + __shfl_xor(l_run[j], 32);
+    if (qrow[j] < 0) continue;
+    const size_t row = (size_t)qrow[j];
+    if (direct) {
+      const float inv = l_all > 0.0f ? 1.0f / l_all : 0.0f;
+      T* dst = static_cast<T*>(p.out) + row * kD;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = o[j][dt][q4 * 4 + r] * inv;
+          store_out<T>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+        }
+      }
+      if (p.lse && hf == 0)
+        p.lse[row] = l_all > 0.0f ? (m_run[j] * p.c2 + __log2f(l_all)) * kLn2 : -INFINITY;
+    } else {
+      const size_t prow = (size_t)ch * ((size_t)p.total_nodes * p.hq) + row;
+      float* dst = p.ws_o + prow * kD;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = o[j][dt][q4 * 4 + r];
+          store_out<float>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+        }
+      }
+      if (hf == 0) {
+        p.ws_m[prow] = l_all > 0.0f ? m_run[j] * p.c2 : -INFINITY;
+        p.ws_l[prow] = l_all;
+      }
+    }
+  }
+}
+
+// Log-sum-exp reduction of the split partials of every output row (rows of
+// single-split requests were finalised by the attention kernel). 32 threads
+// per row, 4 dims each.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p) {
+  const int total_rows = p.total_nodes * p.hq;
+  const int row = blockIdx.x * (kThreads / 32) + (threadIdx.x >> 5);
+  if (row >= total_rows) return;
+  const int node = row / p.hq;
+  // request of this node: last b with node_indptr[b] <= node
+  int lo = 0, hi = p.batch - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.node_indptr[mid] <= node) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo;
+  const int Cb = clampi(p.ctx_len[b], 0, p.max_ctx);
+  const int n_ch_b = max(1, ceil_div(Cb, p.split));
+  if (n_ch_b == 1) return;
+  const size_t stride = (size_t)p.total_nodes * p.hq;
+  float M = -INFINITY;
+  for (int s = 0; s < n_ch_b; ++s) M = fmaxf(M, p.ws_m[s * stride + row]);
+  const float Mu = M == -INFINITY ? 0.0f : M;
+  const int d0 = (threadIdx.x & 31) * 4;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  float L = 0.0f;
+  for (int s = 0; s < n_ch_b; ++s) {
+    const size_t pr = s * stride + row;
+    const float w = __builtin_amdgcn_exp2f(p.ws_m[pr] - Mu);
+    L += w * p.ws_l[pr];
+    const float4 v = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0);
+    acc[0] += w * v.x; acc[1] += w * v.y; acc[2] += w * v.z; acc[3] += w * v.w;
+  }
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  float v[4] = {acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
+  store_out<T>(static_cast<T*>(p.out) + (size_t)row * kD + d0, v);
+  if (p.lse && (threadIdx.x & 31) == 0) p.lse[row] = L > 0.0f ? (M + __log2f(L)) * kLn2 : -INFINITY;
+}
+
+// a5 as a standalone operator: merge two normalised states.
+__global__ __launch_bounds__(kThreads) void merge_state_kernel(int rows, int D, const float* o_a,
+                                                               const float* lse_a, const float* o_b,
+                                                               const float* lse_b, float* o_out,
+                                                               float* lse_out) {
+  const int row = blockIdx.x;
+  if (row >= rows) return;
+  const float la = lse_a[row], lb = lse_b[row];
+  const float m = fmaxf(la, lb);
+  float wa = 0.f, wb = 0.f, lse = -INFINITY;
+  if (m != -INFINITY) {
+    wa = expf(la - m);
+    wb = expf(lb - m);
+    const float s = wa + wb;
+    wa /= s;
+    wb /= s;
+    lse = m + logf(s);
+  }
+  for (int d = threadIdx.x; d < D; d += blockDim.x) {
+    const size_t i = (size_t)row * D + d;
+    o_out[i] = wa * o_a[i] + wb * o_b[i];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) lse_out[row] = lse;
+}
+
+Params make_params(const d2sd_attn_args& a, const AttnPlan& plan, void* ws) {
+  Params p{};
+  p.q = a.q; p.k_cache = a.k_cache; p.v_cache = a.v_cache; p.page_table = a.page_table;
+  p.ctx_len = a.ctx_len; p.k_tree = a.k_tree; p.v_tree = a.v_tree; p.node_indptr = a.node_indptr;
+  p.anc_mask = a.anc_mask; p.out = a.out; p.lse = a.lse;
+  const size_t rows = (size_t)a.total_nodes * a.num_qo_heads;
+  float* w = static_cast<float*>(ws);
+  p.ws_o = w;
+  p.ws_m = w ? w + (size_t)plan.n_ch_max * rows * kD : nullptr;
+  p.ws_l = w ? p.ws_m + (size_t)plan.n_ch_max * rows : nullptr;
+  p.batch = a.batch; p.hq = a.num_qo_heads; p.hkv = a.num_kv_heads; p.G = plan.G; p.stage = a.stage;
+  p.total_nodes = a.total_nodes; p.max_nodes = a.max_nodes; p.max_ctx = a.max_ctx_len;
+  p.num_pages = a.num_pages; p.max_pages = a.max_pages; p.mask_words = a.mask_words;
+  p.split = plan.split; p.n_ch_max = plan.n_ch_max; p.n_rg_max = plan.n_rg_max;
+  p.items = (int)plan.items;
+  p.c2 = plan.scale * kLog2e;
+  return p;
+}
+
+}  // namespace
+
+hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& plan, void* ws,
+                                    hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  const Params p = make_params(a, plan, ws);
+  const int grid = (int)(((plan.items + 7) / 8) * 8);
+  if (ev0) (void)hipEventRecord(ev0, stream);
+  if (a.dtype == D2SD_BF16)
+    hipLaunchKernelGGL(cascade_attention_kernel<__bf16>, dim3(grid), dim3(kThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
+  if (ev1) (void)hipEventRecord(ev1, stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || plan.n_ch_max <= 1) return e;
+  const long long rows = (long long)a.total_nodes * a.num_qo_heads;
+  const int mgrid = (int)((rows + (kThreads / 32) - 1) / (kThreads / 32));
+  if (a.dtype == D2SD_BF16)
+    hipLaunchKernelGGL(split_merge_kernel<__bf16>, dim3(mgrid), dim3(kThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(split_merge_kernel<float>, dim3(mgrid), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hipStream_t stream,
+                                       hipEvent_t ev0, hipEvent_t ev1) {
+  AttnPlan plan{};
+  plan.G = a.num_qo_heads / a.num_kv_heads;
+  plan.split = 1 << 30;  // whole context in one pass
+  plan.n_ch_max = 1;
+  plan.n_rg_max = 1;
+  plan.items = (long long)a.batch * a.num_kv_heads * a.max_nodes;
+  plan.scale = scale;
+  Params p = make_params(a, plan, nullptr);
+  p.node_mode = 1;
+  const int grid = (int)(((plan.items + 7) / 8) * 8);
+  if (ev0) (void)hipEventRecord(ev0, stream);
+  if (a.dtype == D2SD_BF16)
+    hipLaunchKernelGGL(cascade_attention_kernel<__bf16>, dim3(grid), dim3(kThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
+  if (ev1) (void)hipEventRecord(ev1, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,
+                              const float* o_b, const float* lse_b, float* o_out, float* lse_out,
+                              hipStream_t stream) {
+  const int threads = head_dim >= 256 ? 256 : ((head_dim + 63) / 64) * 64;
+  hipLaunchKernelGGL(merge_state_kernel, dim3(rows), dim3(threads), 0, stream, rows, head_dim, o_a,
+                     lse_a, o_b, lse_b, o_out, lse_out);
+  return hipGetLastError();
+}
+
+}  // namespace d2sd

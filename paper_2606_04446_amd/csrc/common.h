@@ -1,0 +1,71 @@
+// Internal definitions shared by the libd2sd translation units (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "d2sd.h"
+
+namespace d2sd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+__host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Bits [lo, hi) of a bit set restricted to word w (bits 32w .. 32w+31).
+__device__ __forceinline__ uint32_t range_bits(int lo, int hi, int w) {
+  const int a = max(lo, 32 * w) - 32 * w;
+  const int e = min(hi, 32 * w + 32) - 32 * w;
+  if (a >= e) return 0u;
+  const uint32_t ones = (e - a) == 32 ? 0xffffffffu : ((1u << (e - a)) - 1u);
+  return ones << a;
+}
+
+// Launchers implemented in the .hip files; the C ABI in api.hip validates first.
+hipError_t launch_tree_build(int batch, int B, int Kmax, const int* K, const int* p,
+                             const int* node_indptr, int total_nodes, int mask_words, int* parent,
+                             int* depth, int* path_id, uint32_t* anc_mask, int* path_leaf,
+                             hipStream_t stream);
+
+hipError_t launch_accept_path(int batch, int B, const int* node_indptr, int total_nodes,
+                              const int* parent, const int* depth, const int* path_id,
+                              const int* draft, const int* argmax, int* accept_len, int* best_path,
+                              int* accept_node, int* path_nodes, int* out_tokens,
+                              hipStream_t stream);
+
+// Resolved plan of one verify-attention call (host side).
+struct AttnPlan {
+  int G;             // query heads per KV head
+  int split;         // context tokens per split (multiple of 64)
+  int n_ch_max;      // splits of the longest context (>= 1)
+  int n_rg_max;      // row groups of the largest request (>= 1)
+  long long items;   // batch * hkv * n_ch_max * n_rg_max
+  size_t ws_bytes;   // partial-state workspace (0 when n_ch_max == 1)
+  float scale;       // softmax scale
+};
+
+hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& plan, void* ws,
+                                    hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+
+hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hipStream_t stream,
+                                       hipEvent_t ev0, hipEvent_t ev1);
+
+hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,
+                              const float* o_b, const float* lse_b, float* o_out, float* lse_out,
+                              hipStream_t stream);
+
+// Rows (queries) per MFMA column tile, and column tiles per workgroup row
+// group of the cascade kernel (4 waves x 2 tiles for bf16, x 1 for fp32); the
+// host planner and the kernels must agree on them.
+constexpr int kRowsPerTile = 32;
+constexpr int kTilesPerGroup = 8;
+__host__ __device__ constexpr int group_rows(int dtype) {
+  return (dtype == D2SD_BF16 ? 8 : 4) * kRowsPerTile;
+}
+
+}  // namespace d2sd

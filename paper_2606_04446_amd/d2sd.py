@@ -1,0 +1,322 @@
+"""Python binding of libd2sd (the C ABI in include/d2sd.h).
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+torch supplies device memory and the stream (``torch.cuda.current_stream()``
+unless one is given). Function names are the C names without the ``d2sd_``
+prefix. Importing this module fails loudly when libd2sd.so has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+# torch ships its own HIP runtime (same soname as the system one). Loading it
+# first makes libd2sd bind to that single runtime; a second runtime in the
+# process cannot open the device, and torch's streams and device pointers are
+# only valid inside the runtime that created them.
+import torch  # noqa: F401  (must precede the CDLL load below)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libd2sd.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "d2sd.h")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = 0, 1, 2, 3, 4
+F32, BF16 = 0, 1
+STAGE_CASCADE, STAGE_PREFIX, STAGE_TREE = 0, 1, 2
+MAX_B, HEAD_DIM, PAGE_SIZE = 64, 128, 16
+
+
+class D2SDError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {detail or 'error'} (status {status})")
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_04446_amd.build` "
+                      "(the verify path has no fallback)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_c_int, _c_ptr, _c_size = ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
+_c_int_p = ctypes.POINTER(ctypes.c_int)
+
+
+class AttnArgs(ctypes.Structure):
+    """Mirror of d2sd_attn_args (field order and types must match the header)."""
+
+    _fields_ = [
+        ("batch", _c_int), ("num_qo_heads", _c_int), ("num_kv_heads", _c_int), ("head_dim", _c_int),
+        ("page_size", _c_int), ("dtype", _c_int), ("stage", _c_int), ("sm_scale", ctypes.c_float),
+        ("total_nodes", _c_int), ("max_nodes", _c_int), ("max_ctx_len", _c_int), ("num_pages", _c_int),
+        ("max_pages", _c_int), ("mask_words", _c_int), ("kv_split", _c_int),
+        ("q", _c_ptr), ("k_cache", _c_ptr), ("v_cache", _c_ptr), ("page_table", _c_ptr),
+        ("ctx_len", _c_ptr), ("k_tree", _c_ptr), ("v_tree", _c_ptr), ("node_indptr", _c_ptr),
+        ("anc_mask", _c_ptr), ("out", _c_ptr), ("lse", _c_ptr),
+    ]
+
+
+def _sig(name, restype, *argtypes):
+    f = getattr(_lib, name)
+    f.restype = restype
+    f.argtypes = list(argtypes)
+    return f
+
+
+_status_string = _sig("d2sd_status_string", ctypes.c_char_p, _c_int)
+_last_error = _sig("d2sd_last_error", ctypes.c_char_p)
+_version = _sig("d2sd_version", _c_int)
+_mask_words = _sig("d2sd_mask_words", _c_int, _c_int)
+_tree_plan = _sig("d2sd_tree_plan", _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_int_p)
+_tree_build = _sig("d2sd_tree_build", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_int,
+                   _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_ws_size = _sig("d2sd_cascade_workspace_size", _c_int, ctypes.POINTER(AttnArgs), ctypes.POINTER(_c_size))
+_kv_split = _sig("d2sd_cascade_kv_split", _c_int, ctypes.POINTER(AttnArgs), _c_int_p)
+_cascade = _sig("d2sd_cascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr, _c_size, _c_ptr)
+_noncascade = _sig("d2sd_noncascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr)
+_merge = _sig("d2sd_merge_state", _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+              _c_ptr)
+_accept = _sig("d2sd_accept_path", _c_int, _c_int, _c_int, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+               _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_timing_enable = _sig("d2sd_kernel_timing_enable", _c_int, _c_int)
+_timing_collect = _sig("d2sd_kernel_timing_collect", _c_int, _c_int_p, ctypes.POINTER(ctypes.c_double))
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise D2SDError(status, where, _last_error().decode())
+
+
+def header_functions() -> list:
+    """Names of the functions include/d2sd.h declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(d2sd_[a-z_0-9]+)\s*\(", text)))
+
+
+def status_string(status: int) -> str:
+    return _status_string(status).decode()
+
+
+def last_error() -> str:
+    return _last_error().decode()
+
+
+def version() -> int:
+    return _version()
+
+
+def mask_words(B: int) -> int:
+    return _mask_words(B)
+
+
+# ---------------------------------------------------------------- helpers --
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    """Device pointer of a contiguous CUDA tensor (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _host_i32(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+# ------------------------------------------------------------------- tree --
+
+def tree_plan(B: int, K, p):
+    """Host planner: returns (node_indptr int32 [batch+1], mask_words)."""
+    K = _host_i32(K)
+    p = _host_i32(p)
+    if p.ndim == 1:
+        p = p.reshape(len(K), -1)
+    batch, kmax = len(K), (p.shape[1] if p.size else 0)
+    indptr = np.zeros(batch + 1, np.int32)
+    w = ctypes.c_int(0)
+    _check(_tree_plan(batch, B, K.ctypes.data, p.ctypes.data if p.size else None, kmax, indptr.ctypes.data,
+                      ctypes.byref(w)), "d2sd_tree_plan")
+    return indptr, w.value
+
+
+def tree_build(B: int, K, p, node_indptr, total_nodes: int, mask_words_: int, out: dict | None = None,
+               stream=None) -> dict:
+    """Device tree build. K [batch], p [batch, Kmax], node_indptr [batch+1] are
+    int32 device tensors. Returns dict(parent, depth, path_id, anc_mask, path_leaf)."""
+    import torch
+    batch = K.numel()
+    kmax = p.shape[1] if p.dim() == 2 else 0
+    dev = K.device
+    o = out or {}
+    parent = (o["parent"] if "parent" in o else torch.empty(total_nodes, dtype=torch.int32, device=dev))
+    depth = (o["depth"] if "depth" in o else torch.empty(total_nodes, dtype=torch.int32, device=dev))
+    path_id = (o["path_id"] if "path_id" in o else torch.empty(total_nodes, dtype=torch.int32, device=dev))
+    anc_mask = (o["anc_mask"] if "anc_mask" in o else torch.empty((total_nodes, mask_words_), dtype=torch.int32, device=dev))
+    path_leaf = (o["path_leaf"] if "path_leaf" in o else torch.empty((batch, kmax + 1), dtype=torch.int32, device=dev))
+    i32 = torch.int32
+    _check(_tree_build(batch, B, kmax, _dev(K, "K", i32), _dev(p, "p", i32) if kmax else None,
+                       _dev(node_indptr, "node_indptr", i32), total_nodes, mask_words_,
+                       _dev(parent, "parent", i32), _dev(depth, "depth", i32), _dev(path_id, "path_id", i32),
+                       _dev(anc_mask, "anc_mask", i32), _dev(path_leaf, "path_leaf", i32), _stream(stream)),
+           "d2sd_tree_build")
+    return dict(parent=parent, depth=depth, path_id=path_id, anc_mask=anc_mask, path_leaf=path_leaf)
+
+
+# -------------------------------------------------------------- attention --
+
+def attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse, *,
+              total_nodes: int, max_nodes: int, max_ctx_len: int, stage: int = STAGE_CASCADE,
+              sm_scale: float = 0.0, kv_split: int = 0) -> AttnArgs:
+    """Fill a d2sd_attn_args from tensors (shapes as documented in the header)."""
+    import torch
+    dt = q.dtype
+    code = {torch.float32: F32, torch.bfloat16: BF16}.get(dt)
+    if code is None:
+        raise ValueError(f"q dtype {dt} unsupported (float32 or bfloat16)")
+    i32 = torch.int32
+    a = AttnArgs()
+    a.batch = ctx_len.numel()
+    a.num_qo_heads = q.shape[1]
+    a.num_kv_heads = k_cache.shape[1]
+    a.head_dim = q.shape[2]
+    a.page_size = k_cache.shape[2]
+    a.dtype = code
+    a.stage = stage
+    a.sm_scale = sm_scale
+    a.total_nodes = total_nodes
+    a.max_nodes = max_nodes
+    a.max_ctx_len = max_ctx_len
+    a.num_pages = k_cache.shape[0]
+    a.max_pages = page_table.shape[1]
+    a.mask_words = anc_mask.shape[1] if anc_mask is not None else 0
+    a.kv_split = kv_split
+    a.q = _dev(q, "q", dt)
+    a.k_cache = _dev(k_cache, "k_cache", dt)
+    a.v_cache = _dev(v_cache, "v_cache", dt)
+    a.page_table = _dev(page_table, "page_table", i32)
+    a.ctx_len = _dev(ctx_len, "ctx_len", i32)
+    a.k_tree = _dev(k_tree, "k_tree", dt)
+    a.v_tree = _dev(v_tree, "v_tree", dt)
+    a.node_indptr = _dev(node_indptr, "node_indptr", i32)
+    a.anc_mask = _dev(anc_mask, "anc_mask", i32)
+    a.out = _dev(out, "out", dt)
+    a.lse = _dev(lse, "lse", torch.float32)
+    return a
+
+
+def cascade_workspace_size(args: AttnArgs) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_ws_size(ctypes.byref(args), ctypes.byref(n)), "d2sd_cascade_workspace_size")
+    return n.value
+
+
+def cascade_kv_split(args: AttnArgs) -> int:
+    n = ctypes.c_int(0)
+    _check(_kv_split(ctypes.byref(args), ctypes.byref(n)), "d2sd_cascade_kv_split")
+    return n.value
+
+
+def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask,
+                             *, total_nodes: int, max_nodes: int, max_ctx_len: int, stage: int = STAGE_CASCADE,
+                             sm_scale: float = 0.0, kv_split: int = 0, out=None, lse=None, workspace=None,
+                             want_lse: bool = True, stream=None):
+    """Verify attention; returns (out, lse). The workspace is allocated when not given."""
+    import torch
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[:2], dtype=torch.float32, device=q.device)
+    a = attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse,
+                  total_nodes=total_nodes, max_nodes=max_nodes, max_ctx_len=max_ctx_len, stage=stage,
+                  sm_scale=sm_scale, kv_split=kv_split)
+    need = cascade_workspace_size(a)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_ptr = _dev(workspace, "workspace") if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_cascade(ctypes.byref(a), ws_ptr, ws_len, _stream(stream)), "d2sd_cascade_verify_attention")
+    return out, lse
+
+
+def noncascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr,
+                                anc_mask, *, total_nodes: int, max_nodes: int, max_ctx_len: int,
+                                sm_scale: float = 0.0, out=None, lse=None, want_lse: bool = True, stream=None):
+    """Comparison baseline: same attention, context re-read per tree node."""
+    import torch
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[:2], dtype=torch.float32, device=q.device)
+    a = attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse,
+                  total_nodes=total_nodes, max_nodes=max_nodes, max_ctx_len=max_ctx_len)
+    _check(_noncascade(ctypes.byref(a), _stream(stream)), "d2sd_noncascade_verify_attention")
+    return out, lse
+
+
+def merge_state(o_a, lse_a, o_b, lse_b, o_out=None, lse_out=None, stream=None):
+    """LSE merge of two fp32 states o [rows, D], lse [rows]."""
+    import torch
+    rows, D = o_a.shape
+    f32 = torch.float32
+    o_out = torch.empty_like(o_a) if o_out is None else o_out
+    lse_out = torch.empty_like(lse_a) if lse_out is None else lse_out
+    _check(_merge(rows, D, _dev(o_a, "o_a", f32), _dev(lse_a, "lse_a", f32), _dev(o_b, "o_b", f32),
+                  _dev(lse_b, "lse_b", f32), _dev(o_out, "o_out", f32), _dev(lse_out, "lse_out", f32),
+                  _stream(stream)), "d2sd_merge_state")
+    return o_out, lse_out
+
+
+# ----------------------------------------------------------------- accept --
+
+def accept_path(B: int, node_indptr, total_nodes: int, parent, depth, path_id, draft_tokens, target_argmax,
+                out: dict | None = None, stream=None) -> dict:
+    """Greedy longest accepted path; returns dict of device int32 tensors."""
+    import torch
+    batch = node_indptr.numel() - 1
+    dev = node_indptr.device
+    o = out or {}
+    i32 = torch.int32
+    res = dict(
+        accept_len=(o["accept_len"] if "accept_len" in o else torch.empty(batch, dtype=i32, device=dev)),
+        best_path=(o["best_path"] if "best_path" in o else torch.empty(batch, dtype=i32, device=dev)),
+        accept_node=(o["accept_node"] if "accept_node" in o else torch.empty(batch, dtype=i32, device=dev)),
+        path_nodes=(o["path_nodes"] if "path_nodes" in o else torch.empty((batch, B), dtype=i32, device=dev)),
+        out_tokens=(o["out_tokens"] if "out_tokens" in o else torch.empty((batch, B), dtype=i32, device=dev)),
+    )
+    _check(_accept(batch, B, _dev(node_indptr, "node_indptr", i32), total_nodes, _dev(parent, "parent", i32),
+                   _dev(depth, "depth", i32), _dev(path_id, "path_id", i32),
+                   _dev(draft_tokens, "draft_tokens", i32), _dev(target_argmax, "target_argmax", i32),
+                   _dev(res["accept_len"], "accept_len", i32), _dev(res["best_path"], "best_path", i32),
+                   _dev(res["accept_node"], "accept_node", i32), _dev(res["path_nodes"], "path_nodes", i32),
+                   _dev(res["out_tokens"], "out_tokens", i32), _stream(stream)), "d2sd_accept_path")
+    return res
+
+
+# ---------------------------------------------------------------- timing --
+
+def kernel_timing_enable(on: bool = True):
+    _check(_timing_enable(1 if on else 0), "d2sd_kernel_timing_enable")
+
+
+def kernel_timing_collect():
+    """(launches, total_ms) of the context-streaming kernel since the last collect."""
+    n = ctypes.c_int(0)
+    ms = ctypes.c_double(0.0)
+    _check(_timing_collect(ctypes.byref(n), ctypes.byref(ms)), "d2sd_kernel_timing_collect")
+    return n.value, ms.value

@@ -1,0 +1,174 @@
+"""C ABI on the CPU: the library loads, exports the header, and its host logic
+(planning, sizing, validation) behaves as documented. No call here reaches a
+kernel launch: every device entry point is exercised only on paths that fail
+validation before any HIP call."""
+
+import ctypes
+import math
+
+import numpy as np
+import pytest
+
+from oracle.tree import build_tree, mask_words as oracle_mask_words
+
+d2sd = pytest.importorskip("paper_2606_04446_amd.d2sd")
+lib = d2sd._lib
+
+FAKE = 0x1000  # never dereferenced: validation fails before any launch
+
+
+def test_exports_every_header_function():
+    names = d2sd.header_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    assert d2sd.status_string(0) == "ok"
+    for s in range(1, 5):
+        assert d2sd.status_string(s) not in ("ok", "unknown status")
+    assert d2sd.status_string(99) == "unknown status"
+    assert d2sd.version() >= 100
+
+
+def test_mask_words_matches_oracle():
+    for B in range(2, 65):
+        assert d2sd.mask_words(B) == oracle_mask_words(B)
+    assert d2sd.mask_words(1) == 0 and d2sd.mask_words(65) == 0
+
+
+def test_tree_plan_matches_oracle_node_counts():
+    rng = np.random.default_rng(0)
+    for _ in range(40):
+        B = int(rng.integers(2, 65))
+        batch = int(rng.integers(1, 9))
+        K = rng.integers(0, B, size=batch)
+        kmax = max(1, int(K.max()))
+        p = np.zeros((batch, kmax), np.int32)
+        for b in range(batch):
+            p[b, :K[b]] = rng.permutation(np.arange(1, B))[:K[b]]   # unsorted on purpose
+        ip, w = d2sd.tree_plan(B, K, p)
+        expect = np.concatenate([[0], np.cumsum([build_tree(B, p[b, :K[b]]).N for b in range(batch)])])
+        assert np.array_equal(ip, expect)
+        assert w == oracle_mask_words(B)
+
+
+@pytest.mark.parametrize("B,K,p,msg", [
+    (1, [0], [[0]], "B = 1"),
+    (65, [0], [[0]], "B = 65"),
+    (16, [2], [[3, 3]], "repeated"),
+    (16, [1], [[0]], "outside"),
+    (16, [1], [[16]], "outside"),
+    (4, [4], [[1, 2, 3, 1]], "K = 4"),
+])
+def test_tree_plan_rejects(B, K, p, msg):
+    K = np.asarray(K, np.int32)
+    p = np.asarray(p, np.int32)
+    out = np.full(len(K) + 1, -7, np.int32)
+    st = lib.d2sd_tree_plan(len(K), B, K.ctypes.data, p.ctypes.data, p.shape[1], out.ctypes.data, None)
+    assert st == d2sd.ERR_INVALID_ARG
+    assert msg in d2sd.last_error()
+    assert (out == -7).all()          # outputs untouched on error
+
+
+def test_tree_plan_null_pointer():
+    K = np.zeros(1, np.int32)
+    assert lib.d2sd_tree_plan(1, 4, K.ctypes.data, None, 0, None, None) == d2sd.ERR_INVALID_ARG
+
+
+def test_tree_build_and_accept_validation():
+    f = ctypes.c_void_p(FAKE)
+    assert lib.d2sd_tree_build(0, 16, 1, f, f, f, 10, 5, f, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert lib.d2sd_tree_build(1, 16, 1, f, f, f, 10, 4, f, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert "mask_words" in d2sd.last_error()
+    assert lib.d2sd_tree_build(1, 16, 1, f, f, f, 10, 5, None, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert lib.d2sd_accept_path(1, 1, f, 10, f, f, f, f, f, f, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert lib.d2sd_accept_path(1, 16, f, 10, f, f, f, f, f, None, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert lib.d2sd_merge_state(4, 0, f, f, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert lib.d2sd_merge_state(4, 128, f, None, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
+
+
+def good_args(**kw):
+    a = d2sd.AttnArgs()
+    a.batch, a.num_qo_heads, a.num_kv_heads, a.head_dim, a.page_size = 32, 32, 8, 128, 16
+    a.dtype, a.stage, a.sm_scale = d2sd.BF16, d2sd.STAGE_CASCADE, 0.0
+    a.total_nodes, a.max_nodes, a.max_ctx_len = 32 * 80, 108, 16384
+    a.num_pages, a.max_pages, a.mask_words, a.kv_split = 32 * 1024, 1024, 5, 0
+    for name in ("q", "k_cache", "v_cache", "page_table", "ctx_len", "k_tree", "v_tree", "node_indptr",
+                 "anc_mask", "out"):
+        setattr(a, name, FAKE)
+    a.lse = None
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def ws_size(a):
+    n = ctypes.c_size_t(123)
+    st = d2sd._ws_size(ctypes.byref(a), ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("batch", 0, d2sd.ERR_INVALID_ARG),
+    ("num_kv_heads", 5, d2sd.ERR_INVALID_ARG),
+    ("head_dim", 64, d2sd.ERR_UNSUPPORTED),
+    ("page_size", 32, d2sd.ERR_UNSUPPORTED),
+    ("dtype", 7, d2sd.ERR_INVALID_ARG),
+    ("stage", 3, d2sd.ERR_INVALID_ARG),
+    ("max_nodes", 5000, d2sd.ERR_INVALID_ARG),
+    ("max_ctx_len", 16385 + 1024 * 16, d2sd.ERR_INVALID_ARG),
+    ("kv_split", 100, d2sd.ERR_INVALID_ARG),
+    ("mask_words", 3, d2sd.ERR_INVALID_ARG),
+    ("num_pages", 0, d2sd.ERR_INVALID_ARG),
+])
+def test_attention_validation(field, value, status):
+    a = good_args(**{field: value})
+    assert ws_size(a)[0] == status
+    assert d2sd._cascade(ctypes.byref(a), None, 0, None) == status
+    assert d2sd.last_error()
+
+
+def test_attention_null_pointers():
+    for name in ("q", "k_cache", "page_table", "ctx_len", "k_tree", "node_indptr", "anc_mask", "out"):
+        a = good_args(**{name: None})
+        assert d2sd._cascade(ctypes.byref(a), None, 0, None) == d2sd.ERR_INVALID_ARG, name
+    # the context-only state does not read the mask
+    a = good_args(anc_mask=None, stage=d2sd.STAGE_PREFIX, kv_split=64)
+    assert d2sd._cascade(ctypes.byref(a), None, 0, None) == d2sd.ERR_WORKSPACE_TOO_SMALL
+
+
+def test_workspace_sizing_and_too_small():
+    a = good_args(kv_split=4096)
+    st, n = ws_size(a)
+    assert st == 0
+    rows = a.total_nodes * a.num_qo_heads
+    assert n == 4 * rows * (128 + 2) * 4          # 4 splits of fp32 partial states
+    assert d2sd._cascade(ctypes.byref(a), ctypes.c_void_p(FAKE), n - 1, None) == d2sd.ERR_WORKSPACE_TOO_SMALL
+    assert "need" in d2sd.last_error()
+    a = good_args(kv_split=16384)                  # one split: finalised in place
+    assert ws_size(a) == (0, 0)
+    a = good_args(stage=d2sd.STAGE_TREE, kv_split=64)
+    assert ws_size(a) == (0, 0)
+
+
+def test_automatic_split():
+    a = good_args()
+    s = d2sd.cascade_kv_split(a)
+    assert s % 64 == 0 and 256 <= s <= 16384
+    small = good_args(batch=1, total_nodes=48, max_nodes=48, max_ctx_len=4096, num_pages=256, max_pages=256)
+    s2 = d2sd.cascade_kv_split(small)
+    assert s2 % 64 == 0 and s2 >= 256 and math.ceil(4096 / s2) > 1
+
+
+def test_noncascade_validation():
+    a = good_args(stage=d2sd.STAGE_PREFIX)
+    assert d2sd._noncascade(ctypes.byref(a), None) == d2sd.ERR_INVALID_ARG
+    a = good_args(num_qo_heads=8 * 300, num_kv_heads=8)
+    assert d2sd._noncascade(ctypes.byref(a), None) == d2sd.ERR_UNSUPPORTED
+
+
+def test_timing_collect_empty():
+    d2sd.kernel_timing_enable(False)
+    assert d2sd.kernel_timing_collect() == (0, 0.0)
