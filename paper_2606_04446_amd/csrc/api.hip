@@ -75,6 +75,7 @@ int mask_words_for(int B) {
 
 constexpr int kNumCUs = 256;
 constexpr int kMinSplit = 256;
+constexpr int kMaxSplit = 32768;   // the bf16 kernel stages a split's page ids in LDS
 
 d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
   if (!a) return fail(D2SD_ERR_INVALID_ARG, "args is NULL");
@@ -104,8 +105,9 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
   if (a->max_ctx_len < 0 || (long long)a->max_ctx_len > (long long)a->max_pages * a->page_size)
     return fail(D2SD_ERR_INVALID_ARG, "max_ctx_len %d outside [0, max_pages*page_size = %lld]",
                 a->max_ctx_len, (long long)a->max_pages * a->page_size);
-  if (a->kv_split < 0 || a->kv_split % 64)
-    return fail(D2SD_ERR_INVALID_ARG, "kv_split %d must be 0 or a positive multiple of 64", a->kv_split);
+  if (a->kv_split < 0 || a->kv_split % 64 || a->kv_split > kMaxSplit)
+    return fail(D2SD_ERR_INVALID_ARG, "kv_split %d must be 0 or a multiple of 64 in [64, %d]", a->kv_split,
+                kMaxSplit);
   if (a->stage != D2SD_STAGE_PREFIX && a->mask_words < (a->max_nodes + 31) / 32)
     return fail(D2SD_ERR_INVALID_ARG, "mask_words %d too small for max_nodes %d", a->mask_words,
                 a->max_nodes);
@@ -132,7 +134,7 @@ int choose_split(const d2sd_attn_args* a, int G) {
   const int avg_groups = max(1, (avg_tiles + tiles_per_group - 1) / tiles_per_group);
   const long long base = (long long)a->batch * a->num_kv_heads * avg_groups;
   int splits = (int)((2ll * kNumCUs + base - 1) / base);
-  splits = max(1, min(splits, ctx / kMinSplit));
+  splits = max(max(1, (ctx + kMaxSplit - 1) / kMaxSplit), min(splits, ctx / kMinSplit));
   const int per = (ctx + splits - 1) / splits;
   return ((per + 63) / 64) * 64;
 }
@@ -270,6 +272,8 @@ d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStre
   if (args->num_qo_heads / args->num_kv_heads > d2sd::group_rows(args->dtype))
     return fail(D2SD_ERR_UNSUPPORTED, "the baseline supports at most %d query heads per KV head",
                 d2sd::group_rows(args->dtype));
+  if (args->dtype == D2SD_BF16 && args->max_ctx_len > kMaxSplit)
+    return fail(D2SD_ERR_UNSUPPORTED, "the baseline streams at most %d context tokens per request", kMaxSplit);
   if (args->total_nodes == 0) return ok();
   const float scale = args->sm_scale > 0.0f ? args->sm_scale : 1.0f / sqrtf((float)args->head_dim);
   hipEvent_t e0, e1;

@@ -22,6 +22,12 @@
 // running max in log2 units, running sum) go to the workspace and a second
 // kernel merges them by log-sum-exp; a request with a single split is
 // finalised in place.
+//
+// bf16 kernel: 8 waves (two per SIMD), each owning one 32-query column tile of
+// the workgroup's 256 rows; the two waves sharing a SIMD overlap one's
+// exponentials with the other's matrix work. The running max is only moved
+// (and O, l rescaled) when it grows by more than 2^8, which keeps the rescale
+// off the common path; interior context tiles skip masking entirely.
 #include <math.h>
 
 #include "common.h"
@@ -89,6 +95,10 @@ __device__ __forceinline__ f32x16 mfma(float a, float b, const f32x16& c) {
 }
 
 __device__ __forceinline__ uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
+
+// s_waitcnt vmcnt(0): wait for every outstanding vector-memory access of the
+// wave (gfx9 encoding: vmcnt 0, expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Pointer to the first element of key `kabs` of request b / KV head h, or null
 // when the key lies outside [0, key_end). Context keys go through the page
@@ -528,6 +538,396 @@ __global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 kernel (the hot path): 8 waves, two per SIMD, one 32-query column tile
+// per wave. K/V tiles of 64 keys are copied global -> LDS by the LDS DMA path
+// (global_load_lds_dwordx4: no staging registers, no VALU) into a four-stage
+// ring, so three tiles are in flight while one is consumed. Both tiles keep
+// the natural [key][dim] layout with 16-byte chunks XOR-swizzled by row:
+//   K: chunk c of row r sits at c ^ (r & 15)   (b128 A-operand reads of 16
+//      consecutive keys hit 16 distinct bank groups)
+//   V: chunk c of row r sits at c ^ 4(r & 3)   (transposing b64 reads)
+// V^T fragments for O^T += V^T P^T come from ds_read_b64_tr_b16: in each
+// 16-lane group, lane i points at V[k0 + i/4][d0 + 4(i%4)] and receives keys
+// k0..k0+3 of dim d0 + i, which is the key order of the P^T slots.
+
+namespace bf {
+constexpr int THREADS = 512;
+constexpr int WAVES = THREADS / kWave;
+constexpr int MAX_SPLIT_PAGES = 2048;    // page ids of one context split staged in LDS
+constexpr int KT = 64;                   // keys per tile
+constexpr int ROW_BYTES = kD * 2;        // 256 B per key row
+constexpr int TILE_BYTES = KT * ROW_BYTES;  // 16 KB for K (and for V)
+constexpr int NSTAGE = 4;
+constexpr int DMA_PER_TILE = 4;          // per wave: two 1 KB blocks of K, two of V
+constexpr float kRescaleLog2 = 8.0f;     // move the running max when it grows by > 2^8
+}  // namespace bf
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 lds_b128(const char* base, int off) {
+  return *reinterpret_cast<const uint4*>(base + off);
+}
+__device__ __forceinline__ s16x4 lds_tr16(const char* base, int off) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(base + off));
+}
+__device__ __forceinline__ void dma16(const void* src, char* lds_block) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_block, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0) then s_barrier; the asm statement is also a
+// compiler memory barrier. Waves keep up to n of their own LDS DMAs in flight.
+template <int N>
+__device__ __forceinline__ void sync_keep() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0070 | N);
+  asm volatile("s_barrier" ::: "memory");
+}
+__device__ __forceinline__ void sync_tiles_in_flight(int later_tiles) {
+  if (later_tiles >= 2) sync_keep<2 * bf::DMA_PER_TILE>();
+  else if (later_tiles == 1) sync_keep<bf::DMA_PER_TILE>();
+  else sync_keep<0>();
+}
+
+struct TileSrc {
+  bool tree;
+  int key0;
+  int key_end;
+};
+
+// Per-lane constants of the DMA copy: this wave copies K/V blocks w and w+8
+// (rows 4b .. 4b+3 of the tile, one 16-byte chunk per lane).
+struct DmaLane {
+  int row[2];     // tile row of the lane's chunk in block w, w+8
+  int kcol[2];    // element offset of the logical K chunk to fetch
+  int vcol[2];    // element offset of the logical V chunk to fetch
+};
+
+__device__ __forceinline__ DmaLane dma_lane(int wave, int lane) {
+  DmaLane d;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int blk = wave + 8 * j;
+    const int r = 4 * blk + (lane >> 4);
+    const int p = lane & 15;          // physical chunk written by this lane
+    d.row[j] = r;
+    d.kcol[j] = (p ^ (r & 15)) * 8;
+    d.vcol[j] = (p ^ ((r & 3) << 2)) * 8;
+  }
+  return d;
+}
+
+// Issue the LDS DMA of one K/V tile into a stage (sK, sV: 16 KB each).
+// Rows past the valid keys are copied from row 0 (their scores are masked,
+// so they only need to be finite).
+__device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int h, int node_base,
+                                         const int* s_pid, int c0, const DmaLane& d, char* sK, char* sV) {
+  const __bf16* kc = static_cast<const __bf16*>(p.k_cache);
+  const __bf16* vc = static_cast<const __bf16*>(p.v_cache);
+  const int nvalid = ts.key_end - ts.key0;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int r = d.row[j];
+    const int rs = r < nvalid ? r : 0;
+    size_t rowoff;
+    const __bf16* kb;
+    const __bf16* vb;
+    if (!ts.tree) {
+      const int key = ts.key0 + rs;
+      const int page = s_pid[(key - c0) >> 4];
+      rowoff = (((size_t)page * p.hkv + h) * D2SD_PAGE_SIZE + (key & 15)) * kD;
+      kb = kc;
+      vb = vc;
+    } else {
+      rowoff = ((size_t)(node_base + ts.key0 + rs) * p.hkv + h) * kD;
+      kb = static_cast<const __bf16*>(p.k_tree);
+      vb = static_cast<const __bf16*>(p.v_tree);
+    }
+    const int blk_off = (wave + 8 * j) * 1024;
+    dma16(kb + rowoff + d.kcol[j], sK + blk_off);
+    dma16(vb + rowoff + d.vcol[j], sV + blk_off);
+  }
+}
+
+// Per-lane LDS read offsets (bytes from the stage base).
+struct ReadLane {
+  int k[8];   // K A-operand chunk of k-step st for key row lane%32 (block 0)
+  int v[4];   // V transposing read for dim tile dt (first 4 keys of k-step 0)
+};
+
+__device__ __forceinline__ ReadLane read_lane(int lane) {
+  ReadLane rl;
+  const int hf = lane >> 5;
+  const int kr = lane & 31;
+#pragma unroll
+  for (int st = 0; st < 8; ++st) rl.k[st] = kr * bf::ROW_BYTES + (((hf * 8 + st) ^ (kr & 15)) << 4);
+  const int grp = lane >> 4;          // 16-lane group: dims (grp&1)*16.., keys +4*(grp>>1)
+  const int i = lane & 15;
+  const int row = 4 * (grp >> 1) + (i >> 2);
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    const int c = dt * 4 + (grp & 1) * 2 + ((i & 3) >> 1);       // logical 16-byte chunk
+    rl.v[dt] = row * bf::ROW_BYTES + ((c ^ ((row & 3) << 2)) << 4) + ((i & 1) << 3);
+  }
+  return rl;
+}
+
+// S^T of one query tile for a 64-key tile (two 32-key blocks).
+__device__ __forceinline__ void qk_tile(const char* sK, const ReadLane& rl, const bf16x8 (&q)[8],
+                                        f32x16 (&s)[2]) {
+  s[0] = f32x16{};
+  s[1] = f32x16{};
+#pragma unroll
+  for (int st = 0; st < 8; ++st) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, lds_b128(sK, rl.k[st] + kb * 32 * bf::ROW_BYTES));
+      s[kb] = mfma(a, q[st], s[kb]);
+    }
+  }
+}
+
+// O^T += V^T P^T over a 64-key tile (4 k-steps of 16 keys).
+__device__ __forceinline__ void pv_tile(const char* sV, const ReadLane& rl, const bf16x8 (&pf)[4],
+                                        f32x16 (&o)[4]) {
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const s16x4 lo = lds_tr16(sV, rl.v[dt] + (ks * 16) * bf::ROW_BYTES);
+      const s16x4 hi = lds_tr16(sV, rl.v[dt] + (ks * 16 + 8) * bf::ROW_BYTES);
+      typedef short s16x8 __attribute__((ext_vector_type(8)));
+      const s16x8 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      o[dt] = mfma(__builtin_bit_cast(bf16x8, a8), pf[ks], o[dt]);
+    }
+  }
+}
+
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Mask keys of a partial or tree tile: slot i of block kb is key
+// 32 kb + (i/4)*8 + hf*4 + i%4 of the tile. `vis` holds the visible keys of
+// the tile; after shifting out the lane half's offset every slot tests a
+// fixed bit.
+__device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int nvalid, uint64_t vis, int hf) {
+  const uint64_t in_range = nvalid >= 64 ? ~0ull : ((1ull << max(nvalid, 0)) - 1ull);
+  const uint64_t m = (vis & in_range) >> (hf * 4);
+  const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int bit = (i >> 2) * 8 + (i & 3);
+    s[0][i] = ((lo >> bit) & 1u) ? s[0][i] : -INFINITY;
+    s[1][i] = ((hi >> bit) & 1u) ? s[1][i] : -INFINITY;
+  }
+}
+
+// Online softmax of one query tile over 64 keys: updates the running max /
+// sum / output scale and leaves bf16 probabilities in B-operand order.
+__device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], float& m_run, float& l_run, f32x16 (&o)[4],
+                                             bf16x8 (&pf)[4], float c2) {
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
+  mx = xhalf_max(mx);
+  const float m_new = fmaxf(m_run, mx);
+  const bool grow = (m_new - m_run) * c2 > bf::kRescaleLog2;  // false when both are -inf
+  if (__ballot(grow)) {
+    const float alpha = m_run == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
+    l_run *= alpha;
+    m_run = m_new;
+  }
+  const float moff = m_run == -INFINITY ? 0.0f : m_run * c2;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float la = 0.0f, lb = 0.0f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      bf16x8 v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * t + j], c2, -moff));
+#pragma unroll
+      for (int j = 0; j < 8; j += 4) {
+        la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v[j], v[j + 1]}, ones, la, false);
+        lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v[j + 2], v[j + 3]}, ones, lb, false);
+      }
+      pf[2 * kb + t] = v;
+    }
+  }
+  l_run += la + lb;
+}
+
+// Visible-key bits of a tree tile for the node of a query row.
+__device__ __forceinline__ uint64_t tree_bits(const Params& p, int node_base, int node, int key0) {
+  const uint32_t* mrow = p.anc_mask + (size_t)(node_base + node) * p.mask_words;
+  const int w0 = key0 >> 5;
+  const uint32_t lo = w0 < p.mask_words ? mrow[w0] : 0u;
+  const uint32_t hi = w0 + 1 < p.mask_words ? mrow[w0 + 1] : 0u;
+  return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+
+__global__ __launch_bounds__(bf::THREADS) void cascade_bf16_kernel(Params p) {
+  constexpr int GROUP_ROWS = bf::WAVES * kRowsPerTile;
+  // four LDS stages as separate arrays (keeps DMA targets and reads apart)
+  __shared__ __attribute__((aligned(1024))) char sk0[bf::TILE_BYTES], sv0[bf::TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char sk1[bf::TILE_BYTES], sv1[bf::TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char sk2[bf::TILE_BYTES], sv2[bf::TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char sk3[bf::TILE_BYTES], sv3[bf::TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) int s_pid[bf::MAX_SPLIT_PAGES + 4];
+
+  // ---- work item (XCD-aware: consecutive items share an XCD and its L2) ----
+  const int per_xcd = gridDim.x / 8;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= p.items) return;
+  int rest = item;
+  int rg = 0, ch = 0, n_sel = 0;
+  if (p.node_mode) {
+    n_sel = rest % p.max_nodes; rest /= p.max_nodes;
+  } else {
+    rg = rest % p.n_rg_max; rest /= p.n_rg_max;
+    ch = rest % p.n_ch_max; rest /= p.n_ch_max;
+  }
+  const int h = rest % p.hkv;
+  const int b = rest / p.hkv;
+  const int node_base = clampi(p.node_indptr[b], 0, p.total_nodes);
+  const int Nb = clampi(p.node_indptr[b + 1] - node_base, 0, min(p.max_nodes, p.total_nodes - node_base));
+  const int Mb = Nb * p.G;
+  int r_lo, r_hi;
+  if (p.node_mode) {
+    if (n_sel >= Nb) return;
+    r_lo = n_sel * p.G;
+    r_hi = r_lo + p.G;
+  } else {
+    r_lo = rg * GROUP_ROWS;
+    if (r_lo >= Mb) return;
+    r_hi = min(Mb, r_lo + GROUP_ROWS);
+  }
+  const int Cb = clampi(p.ctx_len[b], 0, p.max_ctx);
+  const bool use_ctx = p.stage != D2SD_STAGE_TREE;
+  const bool use_tree = p.stage != D2SD_STAGE_PREFIX;
+  const int n_ch_b = use_ctx ? max(1, ceil_div(Cb, p.split)) : 1;
+  if (ch >= n_ch_b) return;
+  const int c0 = use_ctx ? ch * p.split : 0;
+  const int c1 = use_ctx ? min(Cb, c0 + p.split) : 0;
+  const int n_ctx_tiles = c1 > c0 ? ceil_div(c1 - c0, bf::KT) : 0;
+  const int n_tree_tiles = (use_tree && ch == 0) ? ceil_div(Nb, bf::KT) : 0;
+  const int n_tiles = n_ctx_tiles + n_tree_tiles;
+
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int hf = lane >> 5;
+  const int r = r_lo + wave * kRowsPerTile + (lane & 31);
+  const bool active = r_lo + wave * kRowsPerTile < r_hi;   // wave owns at least one row
+  const bool valid = r < r_hi;
+  const int qnode = valid ? r / p.G : 0;
+  const int qrow = valid ? (node_base + qnode) * p.hq + h * p.G + r % p.G : -1;
+
+  // page ids of this split (the split length is capped so they fit)
+  {
+    const int npg = ceil_div(c1 - c0, D2SD_PAGE_SIZE);
+    const int* pt = p.page_table + (size_t)b * p.max_pages + (c0 >> 4);
+    for (int i = threadIdx.x; i < npg; i += bf::THREADS) s_pid[i] = clampi(pt[i], 0, p.num_pages - 1);
+  }
+  bf16x8 q[8];
+  load_q(p, q, valid ? static_cast<const __bf16*>(p.q) + (size_t)qrow * kD : nullptr, hf);
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.0f;
+  __syncthreads();
+
+  auto src = [&](int j) {
+    TileSrc ts;
+    ts.tree = j >= n_ctx_tiles;
+    ts.key0 = ts.tree ? (j - n_ctx_tiles) * bf::KT : c0 + j * bf::KT;
+    ts.key_end = ts.tree ? Nb : c1;
+    return ts;
+  };
+  const DmaLane dl = dma_lane(wave, lane);
+  const ReadLane rl = read_lane(lane);
+
+  // prologue: tiles 0..2 in flight
+  if (n_tiles > 0) dma_tile(p, src(0), h, node_base, s_pid, c0, dl, sk0, sv0);
+  if (n_tiles > 1) dma_tile(p, src(1), h, node_base, s_pid, c0, dl, sk1, sv1);
+  if (n_tiles > 2) dma_tile(p, src(2), h, node_base, s_pid, c0, dl, sk2, sv2);
+
+  // One tile: wait for its copy (keeping later tiles in flight), queue the
+  // tile three ahead into the stage freed by the previous tile, compute.
+  auto step = [&](int jt, const char* cK, const char* cV, char* nK, char* nV) {
+    sync_tiles_in_flight(min(2, n_tiles - 1 - jt));
+    if (jt + 3 < n_tiles) dma_tile(p, src(jt + 3), h, node_base, s_pid, c0, dl, nK, nV);
+    if (!active) return;
+    const TileSrc ts = src(jt);
+    const int nvalid = ts.key_end - ts.key0;
+    f32x16 s[2];
+    qk_tile(cK, rl, q, s);
+    if (ts.tree || nvalid < bf::KT) {
+      uint64_t vis = ~0ull;
+      if (ts.tree) {
+        vis = tree_bits(p, node_base, qnode, ts.key0);  // waits for in-flight copies too (tree tiles are few)
+      }
+      mask_tile(s, nvalid, vis, hf);
+    }
+    bf16x8 pf[4];
+    softmax_tile(s, m_run, l_run, o, pf, p.c2);
+    pv_tile(cV, rl, pf, o);
+  };
+  for (int jt = 0; jt < n_tiles; jt += 4) {
+    step(jt, sk0, sv0, sk3, sv3);
+    if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
+    if (jt + 2 < n_tiles) step(jt + 2, sk2, sv2, sk1, sv1);
+    if (jt + 3 < n_tiles) step(jt + 3, sk3, sv3, sk2, sv2);
+  }
+
+  // ---- epilogue: finalise (single split) or write the split partial ----
+  if (!active) return;
+  const float l_all = l_run + __shfl_xor(l_run, 32);
+  if (!valid) return;
+  const size_t row = (size_t)qrow;
+  if (n_ch_b == 1) {
+    const float inv = l_all > 0.0f ? 1.0f / l_all : 0.0f;
+    __bf16* dst = static_cast<__bf16*>(p.out) + row * kD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        float v[4];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr] * inv;
+        store_out<__bf16>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+      }
+    }
+    if (p.lse && hf == 0) p.lse[row] = l_all > 0.0f ? (m_run * p.c2 + __log2f(l_all)) * kLn2 : -INFINITY;
+  } else {
+    const size_t prow = (size_t)ch * ((size_t)p.total_nodes * p.hq) + row;
+    float* dst = p.ws_o + prow * kD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        float v[4];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr];
+        store_out<float>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+      }
+    }
+    if (hf == 0) {
+      p.ws_m[prow] = l_all > 0.0f ? m_run * p.c2 : -INFINITY;
+      p.ws_l[prow] = l_all;
+    }
+  }
+}
+
 // Log-sum-exp reduction of the split partials of every output row (rows of
 // single-split requests were finalised by the attention kernel). 32 threads
 // per row, 4 dims each.
@@ -620,7 +1020,7 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
   const int grid = (int)(((plan.items + 7) / 8) * 8);
   if (ev0) (void)hipEventRecord(ev0, stream);
   if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(cascade_attention_kernel<__bf16>, dim3(grid), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
   else
     hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
   if (ev1) (void)hipEventRecord(ev1, stream);
@@ -649,7 +1049,7 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
   const int grid = (int)(((plan.items + 7) / 8) * 8);
   if (ev0) (void)hipEventRecord(ev0, stream);
   if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(cascade_attention_kernel<__bf16>, dim3(grid), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
   else
     hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
   if (ev1) (void)hipEventRecord(ev1, stream);

@@ -60,8 +60,8 @@ hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const fl
                               hipStream_t stream);
 
 // Rows (queries) per MFMA column tile, and column tiles per workgroup row
-// group of the cascade kernel (4 waves x 2 tiles for bf16, x 1 for fp32); the
-// host planner and the kernels must agree on them.
+// group of the cascade kernel (8 waves x 1 tile for bf16, 4 waves x 1 tile for
+// fp32); the host planner and the kernels must agree on them.
 constexpr int kRowsPerTile = 32;
 constexpr int kTilesPerGroup = 8;
 __host__ __device__ constexpr int group_rows(int dtype) {

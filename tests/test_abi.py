@@ -120,6 +120,7 @@ def ws_size(a):
     ("max_nodes", 5000, d2sd.ERR_INVALID_ARG),
     ("max_ctx_len", 16385 + 1024 * 16, d2sd.ERR_INVALID_ARG),
     ("kv_split", 100, d2sd.ERR_INVALID_ARG),
+    ("kv_split", 32768 + 64, d2sd.ERR_INVALID_ARG),
     ("mask_words", 3, d2sd.ERR_INVALID_ARG),
     ("num_pages", 0, d2sd.ERR_INVALID_ARG),
 ])
@@ -166,6 +167,8 @@ def test_noncascade_validation():
     a = good_args(stage=d2sd.STAGE_PREFIX)
     assert d2sd._noncascade(ctypes.byref(a), None) == d2sd.ERR_INVALID_ARG
     a = good_args(num_qo_heads=8 * 300, num_kv_heads=8)
+    assert d2sd._noncascade(ctypes.byref(a), None) == d2sd.ERR_UNSUPPORTED
+    a = good_args(max_ctx_len=32768 + 16, max_pages=4096)
     assert d2sd._noncascade(ctypes.byref(a), None) == d2sd.ERR_UNSUPPORTED
 
 
