@@ -552,14 +552,16 @@ __global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
 // k0..k0+3 of dim d0 + i, which is the key order of the P^T slots.
 
 namespace bf {
-constexpr int THREADS = 512;
-constexpr int WAVES = THREADS / kWave;
+constexpr int WAVES = kBf16Waves;        // waves per workgroup, one 32-query tile each
+constexpr int THREADS = WAVES * kWave;
 constexpr int MAX_SPLIT_PAGES = 2048;    // page ids of one context split staged in LDS
 constexpr int KT = 64;                   // keys per tile
 constexpr int ROW_BYTES = kD * 2;        // 256 B per key row
 constexpr int TILE_BYTES = KT * ROW_BYTES;  // 16 KB for K (and for V)
-constexpr int NSTAGE = 4;
-constexpr int DMA_PER_TILE = 4;          // per wave: two 1 KB blocks of K, two of V
+constexpr int NSTAGE = WAVES == 8 ? 4 : 2;  // LDS ring depth (two workgroups per CU fit at 2)
+constexpr int BLOCKS = KT / 4;           // 1 KB (four-row) DMA blocks per K or V tile
+constexpr int WAVE_BLOCKS = BLOCKS / WAVES;   // K (and V) blocks copied by each wave
+constexpr int DMA_PER_TILE = 2 * WAVE_BLOCKS; // DMA instructions per wave per tile
 constexpr float kRescaleLog2 = 8.0f;     // move the running max when it grows by > 2^8
 }  // namespace bf
 
@@ -580,13 +582,16 @@ __device__ __forceinline__ void dma16(const void* src, char* lds_block) {
 // compiler memory barrier. Waves keep up to n of their own LDS DMAs in flight.
 template <int N>
 __device__ __forceinline__ void sync_keep() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0070 | N);
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]
+  __builtin_amdgcn_s_waitcnt((N & 15) | 0x0070 | ((N >> 4) << 14));
   asm volatile("s_barrier" ::: "memory");
 }
+// Wait until the oldest tile's copy is complete while `later_tiles` younger
+// tiles (at most NSTAGE - 2) stay in flight, then barrier.
 __device__ __forceinline__ void sync_tiles_in_flight(int later_tiles) {
-  if (later_tiles >= 2) sync_keep<2 * bf::DMA_PER_TILE>();
-  else if (later_tiles == 1) sync_keep<bf::DMA_PER_TILE>();
+  if (bf::NSTAGE > 3 && later_tiles >= 2) sync_keep<2 * bf::DMA_PER_TILE>();
+  else if (bf::NSTAGE > 2 && later_tiles >= 1) sync_keep<bf::DMA_PER_TILE>();
   else sync_keep<0>();
 }
 
@@ -596,19 +601,19 @@ struct TileSrc {
   int key_end;
 };
 
-// Per-lane constants of the DMA copy: this wave copies K/V blocks w and w+8
-// (rows 4b .. 4b+3 of the tile, one 16-byte chunk per lane).
+// Per-lane constants of the DMA copy: this wave copies K/V blocks
+// w, w + WAVES, ... (rows 4b .. 4b+3 of the tile, one 16-byte chunk per lane).
 struct DmaLane {
-  int row[2];     // tile row of the lane's chunk in block w, w+8
-  int kcol[2];    // element offset of the logical K chunk to fetch
-  int vcol[2];    // element offset of the logical V chunk to fetch
+  int row[bf::WAVE_BLOCKS];   // tile row of the lane's chunk in each block
+  int kcol[bf::WAVE_BLOCKS];  // element offset of the logical K chunk to fetch
+  int vcol[bf::WAVE_BLOCKS];  // element offset of the logical V chunk to fetch
 };
 
 __device__ __forceinline__ DmaLane dma_lane(int wave, int lane) {
   DmaLane d;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int blk = wave + 8 * j;
+  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
+    const int blk = wave + bf::WAVES * j;
     const int r = 4 * blk + (lane >> 4);
     const int p = lane & 15;          // physical chunk written by this lane
     d.row[j] = r;
@@ -628,7 +633,7 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
   const int nvalid = ts.key_end - ts.key0;
   const int wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
     const int r = d.row[j];
     const int rs = r < nvalid ? r : 0;
     size_t rowoff;
@@ -645,7 +650,7 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
       kb = static_cast<const __bf16*>(p.k_tree);
       vb = static_cast<const __bf16*>(p.v_tree);
     }
-    const int blk_off = (wave + 8 * j) * 1024;
+    const int blk_off = (wave + bf::WAVES * j) * 1024;
     dma16(kb + rowoff + d.kcol[j], sK + blk_off);
     dma16(vb + rowoff + d.vcol[j], sV + blk_off);
   }
@@ -776,13 +781,16 @@ __device__ __forceinline__ uint64_t tree_bits(const Params& p, int node_base, in
   return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
-__global__ __launch_bounds__(bf::THREADS) void cascade_bf16_kernel(Params p) {
+__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(bf::WAVES == 4 ? 2 : 1)))
+void cascade_bf16_kernel(Params p) {
   constexpr int GROUP_ROWS = bf::WAVES * kRowsPerTile;
-  // four LDS stages as separate arrays (keeps DMA targets and reads apart)
+  // LDS ring stages as separate arrays (keeps DMA targets and reads apart)
   __shared__ __attribute__((aligned(1024))) char sk0[bf::TILE_BYTES], sv0[bf::TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char sk1[bf::TILE_BYTES], sv1[bf::TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char sk2[bf::TILE_BYTES], sv2[bf::TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char sk3[bf::TILE_BYTES], sv3[bf::TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char sk2[bf::NSTAGE > 2 ? bf::TILE_BYTES : 16];
+  __shared__ __attribute__((aligned(1024))) char sv2[bf::NSTAGE > 2 ? bf::TILE_BYTES : 16];
+  __shared__ __attribute__((aligned(1024))) char sk3[bf::NSTAGE > 3 ? bf::TILE_BYTES : 16];
+  __shared__ __attribute__((aligned(1024))) char sv3[bf::NSTAGE > 3 ? bf::TILE_BYTES : 16];
   __shared__ __attribute__((aligned(16))) int s_pid[bf::MAX_SPLIT_PAGES + 4];
 
   // ---- work item (XCD-aware: consecutive items share an XCD and its L2) ----
@@ -856,16 +864,17 @@ __global__ __launch_bounds__(bf::THREADS) void cascade_bf16_kernel(Params p) {
   const DmaLane dl = dma_lane(wave, lane);
   const ReadLane rl = read_lane(lane);
 
-  // prologue: tiles 0..2 in flight
+  // prologue: tiles 0 .. NSTAGE-2 in flight
+  constexpr int AHEAD = bf::NSTAGE - 1;
   if (n_tiles > 0) dma_tile(p, src(0), h, node_base, s_pid, c0, dl, sk0, sv0);
-  if (n_tiles > 1) dma_tile(p, src(1), h, node_base, s_pid, c0, dl, sk1, sv1);
-  if (n_tiles > 2) dma_tile(p, src(2), h, node_base, s_pid, c0, dl, sk2, sv2);
+  if (AHEAD > 1 && n_tiles > 1) dma_tile(p, src(1), h, node_base, s_pid, c0, dl, sk1, sv1);
+  if (AHEAD > 2 && n_tiles > 2) dma_tile(p, src(2), h, node_base, s_pid, c0, dl, sk2, sv2);
 
   // One tile: wait for its copy (keeping later tiles in flight), queue the
-  // tile three ahead into the stage freed by the previous tile, compute.
+  // tile NSTAGE-1 ahead into the stage freed by the previous tile, compute.
   auto step = [&](int jt, const char* cK, const char* cV, char* nK, char* nV) {
-    sync_tiles_in_flight(min(2, n_tiles - 1 - jt));
-    if (jt + 3 < n_tiles) dma_tile(p, src(jt + 3), h, node_base, s_pid, c0, dl, nK, nV);
+    sync_tiles_in_flight(min(AHEAD - 1, n_tiles - 1 - jt));
+    if (jt + AHEAD < n_tiles) dma_tile(p, src(jt + AHEAD), h, node_base, s_pid, c0, dl, nK, nV);
     if (!active) return;
     const TileSrc ts = src(jt);
     const int nvalid = ts.key_end - ts.key0;
@@ -882,11 +891,18 @@ __global__ __launch_bounds__(bf::THREADS) void cascade_bf16_kernel(Params p) {
     softmax_tile(s, m_run, l_run, o, pf, p.c2);
     pv_tile(cV, rl, pf, o);
   };
-  for (int jt = 0; jt < n_tiles; jt += 4) {
-    step(jt, sk0, sv0, sk3, sv3);
-    if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
-    if (jt + 2 < n_tiles) step(jt + 2, sk2, sv2, sk1, sv1);
-    if (jt + 3 < n_tiles) step(jt + 3, sk3, sv3, sk2, sv2);
+  if constexpr (bf::NSTAGE == 4) {
+    for (int jt = 0; jt < n_tiles; jt += 4) {
+      step(jt, sk0, sv0, sk3, sv3);
+      if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
+      if (jt + 2 < n_tiles) step(jt + 2, sk2, sv2, sk1, sv1);
+      if (jt + 3 < n_tiles) step(jt + 3, sk3, sv3, sk2, sv2);
+    }
+  } else {
+    for (int jt = 0; jt < n_tiles; jt += 2) {
+      step(jt, sk0, sv0, sk1, sv1);
+      if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
+    }
   }
 
   // ---- epilogue: finalise (single split) or write the split partial ----

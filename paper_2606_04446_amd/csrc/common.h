@@ -59,13 +59,22 @@ hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const fl
                               const float* o_b, const float* lse_b, float* o_out, float* lse_out,
                               hipStream_t stream);
 
-// Rows (queries) per MFMA column tile, and column tiles per workgroup row
-// group of the cascade kernel (8 waves x 1 tile for bf16, 4 waves x 1 tile for
-// fp32); the host planner and the kernels must agree on them.
+// Waves (one 32-query column tile each) per workgroup of the bf16 kernel.
+// Four waves let two workgroups share a CU, so one computes while the other
+// waits on its barrier or its copies.
+#ifndef D2SD_BF16_WAVES
+#define D2SD_BF16_WAVES 4
+#endif
+constexpr int kBf16Waves = D2SD_BF16_WAVES;
+static_assert(kBf16Waves == 4 || kBf16Waves == 8, "bf16 workgroup size");
+
+// Rows (queries) per MFMA column tile, and rows per workgroup row group of
+// the cascade kernel (one tile per wave: kBf16Waves for bf16, 4 for fp32);
+// the host planner and the kernels must agree on them.
 constexpr int kRowsPerTile = 32;
 constexpr int kTilesPerGroup = 8;
 __host__ __device__ constexpr int group_rows(int dtype) {
-  return (dtype == D2SD_BF16 ? 8 : 4) * kRowsPerTile;
+  return (dtype == D2SD_BF16 ? kBf16Waves : 4) * kRowsPerTile;
 }
 
 }  // namespace d2sd
