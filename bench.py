@@ -3,6 +3,7 @@ attention -> accept path, on a seeded synthetic batch resident in HBM.
 
     python bench.py [--steps K] [--warmup W] [--config 4] [--kv-split S]
                     [--cpu-seconds 15] [--no-cpu-baseline] [--noncascade]
+    python bench.py --copy-probe       (HBM counter calibration copy)
 
 Prints one JSON line. value = verified tree tokens per second of the whole
 step (tree nodes verified / step time). The roofline object describes the
@@ -27,7 +28,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix peaks
 METRIC = "verified tree tokens/sec + prefix-KV HBM GB/s (% of peak), cascade verify attn"
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_04446_amd", "csrc", "attention.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_04446_amd", "csrc", f) for f in ("attention.hip", "common.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cascade_attention_traffic.json")
 
 
@@ -41,15 +42,40 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--noncascade", action="store_true", help="also time the non-cascade baseline kernel")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy three times (HBM counter calibration)")
     return ap.parse_args()
 
 
+def copy_probe():
+    """A device copy of known size: its FETCH_SIZE / WRITE_SIZE counters give
+    the factor between those counters and the bytes actually moved."""
+    import torch
+
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
+
+
 def kernel_sha() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the attention kernel sources with comments and blank lines
+    removed (a comment edit does not invalidate recorded counters)."""
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path) as f:
+            for line in f:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
+    return h.hexdigest()[:16]
 
 
-def measured_traffic(config: int, kv_split: int):
+def measured_traffic(config: int, kv_split: int, resolved_split: int):
     """HBM bytes per launch from committed rocprofv3 counters, if they were taken
     on the current kernel source and the same launch configuration."""
     try:
@@ -59,7 +85,8 @@ def measured_traffic(config: int, kv_split: int):
         return None
     key = f"config{config}"
     r = rec.get(key)
-    if not r or r.get("kernel_sha") != kernel_sha() or r.get("kv_split") != kv_split:
+    if not r or r.get("kernel_sha") != kernel_sha() or r.get("kv_split") != kv_split \
+            or r.get("resolved_kv_split") != resolved_split:
         return None
     return r.get("hbm_bytes_per_launch")
 
@@ -110,6 +137,9 @@ def main():
         print(f"bench.py measures one GPU only (the verify path is built and measured on a single "
               f"MI355X); --gpus {args.gpus} / WORLD_SIZE {world} is not supported", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
 
     import torch
 
@@ -185,7 +215,7 @@ def main():
     tflops = flops / t_s / 1e12
     t_hbm = prefix_bytes / (HBM_PEAK_GBPS * 1e9)
     t_mfma = flops / (MFMA_PEAK_TFLOPS[spec.dtype] * 1e12)
-    traffic = measured_traffic(args.config, kv_split)
+    traffic = measured_traffic(args.config, args.kv_split, kv_split)
     if t_mfma > t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_PEAK_TFLOPS[spec.dtype],
                 "unit": "TFLOP/s", "frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4), "traffic": traffic}

@@ -85,7 +85,7 @@ const char* d2sd_last_error(void);
 /* Library version as major*10000 + minor*100 + patch. */
 int d2sd_version(void);
 
-/* ------------------------------------------------------- a1: tree build -- */
+/* ------------------------------------------------------------ tree build -- */
 
 /* Number of 32-bit words in one ancestor-mask row for block length B:
  * ceil((B + B(B-1)/2) / 32), the largest node count any p set can produce
@@ -137,7 +137,7 @@ d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int*
                             int* parent, int* depth, int* path_id, uint32_t* anc_mask,
                             int* path_leaf, hipStream_t stream);
 
-/* ------------------------------------------ a2-a5: cascade verify attention -- */
+/* ----------------------------------------------- cascade verify attention -- */
 
 /*
  * Arguments of the verify attention (sec. 3.3 (iv): the target verifies the
@@ -237,7 +237,7 @@ d2sd_status d2sd_merge_state(int rows, int head_dim, const float* o_a, const flo
  */
 d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStream_t stream);
 
-/* ----------------------------------------------------- a6: accept path -- */
+/* ----------------------------------------------------------- accept path -- */
 
 /*
  * Device. Greedy longest-accepted-prefix search across the candidate tree and

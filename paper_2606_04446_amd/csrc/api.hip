@@ -121,9 +121,10 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
 }
 
 // Context tokens per split. Automatic choice: enough (request, KV head, row
-// group, split) work items for about two workgroups per CU, but no split
-// shorter than kMinSplit tokens (the partial state of a split costs as many
-// bytes as ~M/2 keys of K/V, M = rows sharing it).
+// group, split) work items for about two rounds of resident workgroups (two
+// per CU for the 4-wave bf16 kernel, one otherwise), but no split shorter
+// than kMinSplit tokens (the partial state of a split costs as many bytes as
+// ~M/2 keys of K/V, M = rows sharing it).
 int choose_split(const d2sd_attn_args* a, int G) {
   if (a->kv_split > 0) return a->kv_split;
   const int ctx = a->max_ctx_len;
@@ -133,7 +134,8 @@ int choose_split(const d2sd_attn_args* a, int G) {
   const int tiles_per_group = d2sd::group_rows(a->dtype) / d2sd::kRowsPerTile;
   const int avg_groups = max(1, (avg_tiles + tiles_per_group - 1) / tiles_per_group);
   const long long base = (long long)a->batch * a->num_kv_heads * avg_groups;
-  int splits = (int)((2ll * kNumCUs + base - 1) / base);
+  const int resident = kNumCUs * (a->dtype == D2SD_BF16 && d2sd::kBf16Waves == 4 ? 2 : 1);
+  int splits = (int)((2ll * resident + base - 1) / base);
   splits = max(max(1, (ctx + kMaxSplit - 1) / kMaxSplit), min(splits, ctx / kMinSplit));
   const int per = (ctx + splits - 1) / splits;
   return ((per + 63) / 64) * 64;

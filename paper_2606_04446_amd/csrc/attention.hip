@@ -983,7 +983,7 @@ __global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p) {
   if (p.lse && (threadIdx.x & 31) == 0) p.lse[row] = L > 0.0f ? (M + __log2f(L)) * kLn2 : -INFINITY;
 }
 
-// a5 as a standalone operator: merge two normalised states.
+// The cascade merge as a standalone operator: merge two normalised states.
 __global__ __launch_bounds__(kThreads) void merge_state_kernel(int rows, int D, const float* o_a,
                                                                const float* lse_a, const float* o_b,
                                                                const float* lse_b, float* o_out,
