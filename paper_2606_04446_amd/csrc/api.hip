@@ -102,6 +102,9 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
     return fail(D2SD_ERR_UNSUPPORTED, "total_nodes * num_qo_heads exceeds 2^30 rows");
   if (a->max_pages < 1 || a->num_pages < 1)
     return fail(D2SD_ERR_INVALID_ARG, "max_pages and num_pages must be >= 1");
+  if ((long long)a->num_pages * a->num_kv_heads > 0x7fffffffll)
+    return fail(D2SD_ERR_UNSUPPORTED, "num_pages x num_kv_heads = %lld exceeds 2^31 - 1",
+                (long long)a->num_pages * a->num_kv_heads);
   if (a->max_ctx_len < 0 || (long long)a->max_ctx_len > (long long)a->max_pages * a->page_size)
     return fail(D2SD_ERR_INVALID_ARG, "max_ctx_len %d outside [0, max_pages*page_size = %lld]",
                 a->max_ctx_len, (long long)a->max_pages * a->page_size);

@@ -574,8 +574,27 @@ __device__ __forceinline__ s16x4 lds_tr16(const char* base, int off) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (__attribute__((address_space(3))) s16x4*)(base + off));
 }
-__device__ __forceinline__ void dma16(const void* src, char* lds_block) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_block, 16, 0, 0);
+// LDS DMA copies are issued as inline asm so that the compiler does not
+// track them: its own tracking cannot tell ring stages apart and would make
+// every later LDS read wait for all copies in flight (vmcnt(0)). The kernel
+// orders copies and reads itself (sync_keep); untracked loads can only
+// lengthen the compiler's own vmcnt waits, never shorten them. The s_nop
+// covers the M0-write to LDS-DMA hazard. Each lane's 16 bytes land at
+// M0 + 16 * lane.
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
+}
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma16s(const char* base, uint32_t lane_off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(lane_off), "s"(base), "s"(lds)
+               : "memory", "m0");
 }
 
 // s_waitcnt vmcnt(n) lgkmcnt(0) then s_barrier; the asm statement is also a
@@ -641,8 +660,8 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
     const __bf16* vb;
     if (!ts.tree) {
       const int key = ts.key0 + rs;
-      const int page = s_pid[(key - c0) >> 4];
-      rowoff = (((size_t)page * p.hkv + h) * D2SD_PAGE_SIZE + (key & 15)) * kD;
+      const int ph = s_pid[(key - c0) >> 4];
+      rowoff = ((size_t)ph * D2SD_PAGE_SIZE + (key & 15)) * kD;
       kb = kc;
       vb = vc;
     } else {
@@ -650,9 +669,30 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
       kb = static_cast<const __bf16*>(p.k_tree);
       vb = static_cast<const __bf16*>(p.v_tree);
     }
-    const int blk_off = (wave + bf::WAVES * j) * 1024;
-    dma16(kb + rowoff + d.kcol[j], sK + blk_off);
-    dma16(vb + rowoff + d.vcol[j], sV + blk_off);
+    const uint32_t blk_off = (uint32_t)__builtin_amdgcn_readfirstlane(wave + bf::WAVES * j) * 1024u;
+    dma16(kb + rowoff + d.kcol[j], lds_addr(sK) + blk_off);
+    dma16(vb + rowoff + d.vcol[j], lds_addr(sV) + blk_off);
+  }
+}
+// Fast copy of a full context tile. A four-row block lies in one page (tiles
+// start on page boundaries), so its source is a wave-uniform page base plus a
+// per-lane offset that depends only on the lane and the block's row within
+// the page, which is the same for every block of a wave.
+__device__ __forceinline__ void dma_ctx_tile(const Params& p, int key0, int c0, const int* s_pid, int wave_s,
+                                             uint32_t koff, uint32_t voff, const char* sK, const char* sV) {
+  const char* kc = static_cast<const char*>(p.k_cache);
+  const char* vc = static_cast<const char*>(p.v_cache);
+  const int pg0 = (key0 - c0) >> 4;
+  uint32_t ph[bf::WAVE_BLOCKS];               // page * hkv + h of each block (read first: one LDS wait)
+#pragma unroll
+  for (int j = 0; j < bf::WAVE_BLOCKS; ++j)
+    ph[j] = (uint32_t)__builtin_amdgcn_readfirstlane(s_pid[pg0 + ((wave_s + bf::WAVES * j) >> 2)]);
+#pragma unroll
+  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
+    const uint32_t blk = wave_s + bf::WAVES * j;
+    const size_t off = (size_t)ph[j] << 12;    // 16 rows x 256 B per (page, KV head)
+    dma16s(kc + off, koff, lds_addr(sK) + blk * 1024u);
+    dma16s(vc + off, voff, lds_addr(sV) + blk * 1024u);
   }
 }
 
@@ -844,7 +884,7 @@ void cascade_bf16_kernel(Params p) {
   {
     const int npg = ceil_div(c1 - c0, D2SD_PAGE_SIZE);
     const int* pt = p.page_table + (size_t)b * p.max_pages + (c0 >> 4);
-    for (int i = threadIdx.x; i < npg; i += bf::THREADS) s_pid[i] = clampi(pt[i], 0, p.num_pages - 1);
+    for (int i = threadIdx.x; i < npg; i += bf::THREADS) s_pid[i] = clampi(pt[i], 0, p.num_pages - 1) * p.hkv + h;
   }
   bf16x8 q[8];
   load_q(p, q, valid ? static_cast<const __bf16*>(p.q) + (size_t)qrow * kD : nullptr, hf);
@@ -852,6 +892,9 @@ void cascade_bf16_kernel(Params p) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.0f;
+  // Retire the Q loads on every path before the first copy is queued: the
+  // compiler's later waits for them would otherwise also wait for the copies.
+  wait_vmem();
   __syncthreads();
 
   auto src = [&](int j) {
@@ -863,18 +906,30 @@ void cascade_bf16_kernel(Params p) {
   };
   const DmaLane dl = dma_lane(wave, lane);
   const ReadLane rl = read_lane(lane);
+  // fast-path lane offsets: row within the page and swizzled source chunk
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const int prow = 4 * (wave & 3) + (lane >> 4);
+  const uint32_t koff = prow * bf::ROW_BYTES + (((lane & 15) ^ prow) << 4);
+  const uint32_t voff = prow * bf::ROW_BYTES + (((lane & 15) ^ ((prow & 3) << 2)) << 4);
+  auto copy_tile = [&](int j, const char* sK, const char* sV) {
+    const TileSrc ts = src(j);
+    if (!ts.tree && ts.key_end - ts.key0 >= bf::KT)
+      dma_ctx_tile(p, ts.key0, c0, s_pid, wave_s, koff, voff, sK, sV);
+    else
+      dma_tile(p, ts, h, node_base, s_pid, c0, dl, const_cast<char*>(sK), const_cast<char*>(sV));
+  };
 
   // prologue: tiles 0 .. NSTAGE-2 in flight
   constexpr int AHEAD = bf::NSTAGE - 1;
-  if (n_tiles > 0) dma_tile(p, src(0), h, node_base, s_pid, c0, dl, sk0, sv0);
-  if (AHEAD > 1 && n_tiles > 1) dma_tile(p, src(1), h, node_base, s_pid, c0, dl, sk1, sv1);
-  if (AHEAD > 2 && n_tiles > 2) dma_tile(p, src(2), h, node_base, s_pid, c0, dl, sk2, sv2);
+  if (n_tiles > 0) copy_tile(0, sk0, sv0);
+  if (AHEAD > 1 && n_tiles > 1) copy_tile(1, sk1, sv1);
+  if (AHEAD > 2 && n_tiles > 2) copy_tile(2, sk2, sv2);
 
   // One tile: wait for its copy (keeping later tiles in flight), queue the
   // tile NSTAGE-1 ahead into the stage freed by the previous tile, compute.
   auto step = [&](int jt, const char* cK, const char* cV, char* nK, char* nV) {
     sync_tiles_in_flight(min(AHEAD - 1, n_tiles - 1 - jt));
-    if (jt + AHEAD < n_tiles) dma_tile(p, src(jt + AHEAD), h, node_base, s_pid, c0, dl, nK, nV);
+    if (jt + AHEAD < n_tiles) copy_tile(jt + AHEAD, nK, nV);
     if (!active) return;
     const TileSrc ts = src(jt);
     const int nvalid = ts.key_end - ts.key0;
