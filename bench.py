@@ -269,6 +269,25 @@ def main():
         res["noncascade"] = {"kernel_ms": round(nc_ms, 3), "speedup_of_cascade": round(nc_ms / kern_ms, 2),
                              "requested_prefix_bytes": int((np.repeat(ctx, n_per_req)).sum()) * Hkv * D * 2 * esz,
                              "max_abs_diff_vs_cascade": float((out2.float() - out.float()).abs().max())}
+    # Device re-anchor selection (Eq. 4-5) and node offsets for the same batch,
+    # the steps that precede the verify path when boundaries come from the
+    # drafter's confidences; timed on their own (they are not in `value`).
+    conf = t(wl.draw_confidences(layout))
+    kmax = max(int(layout.K.max(initial=0)), 1)
+    p_sel = torch.empty((layout.batch, kmax), dtype=torch.int32, device=dev)
+    ip_sel = torch.empty(layout.batch + 1, dtype=torch.int32, device=dev)
+    for _ in range(3):
+        d2sd.select_reanchor(B, conf, d_K, kmax, p_out=p_sel)
+        d2sd.tree_indptr(B, d_K, p_sel, out=ip_sel)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        d2sd.select_reanchor(B, conf, d_K, kmax, p_out=p_sel)
+        d2sd.tree_indptr(B, d_K, p_sel, out=ip_sel)
+    e1.record()
+    torch.cuda.synchronize()
+    res["device_reanchor_us"] = round(e0.elapsed_time(e1) * 1e3 / args.steps, 2)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(x, layout, node_indptr, parent_host, args.cpu_seconds)
     print(json.dumps(res), flush=True)

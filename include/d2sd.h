@@ -137,6 +137,38 @@ d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int*
                             int* parent, int* depth, int* path_id, uint32_t* anc_mask,
                             int* path_leaf, hipStream_t stream);
 
+/*
+ * Device. Re-anchor selection from the first drafter's confidences (sec. 3.1
+ * Eq. 3-4, sec. 3.2 Eq. 5, sec. 3.3 (ii)). For every request b:
+ *   r(i) = (c_1 c_2 ... c_i) (1 - c_{i+1}),  i = 0 .. B-2,
+ * the probability that exactly i drafts are accepted, evaluated in float64 in
+ * that order (product from c_1 upward, then the factor 1 - c_{i+1}, no fused
+ * operations), so the result is reproducible bit for bit. The min(K[b], Kmax,
+ * B-1) largest r(i) are kept, equal values going to the smaller i; prefix
+ * length i gives the re-anchor position p = i + 1.
+ *  conf[batch, B-1]  float32, conf[b, k-1] = c_k in [0, 1] (not checked).
+ *  K[batch]          int32 branch counts (clamped to [0, min(Kmax, B-1)]).
+ *  p_out[batch, Kmax] int32 out: the kept positions in ascending order, then
+ *                    -1 up to Kmax. Feeds d2sd_tree_indptr / d2sd_tree_build.
+ *  r_out[batch, B-1] float64 out (nullable): r(0 .. B-2).
+ * All pointers are device pointers. Errors: INVALID_ARG (nothing launched).
+ */
+d2sd_status d2sd_select_reanchor(int batch, int B, int Kmax, const float* conf, const int* K, int* p_out,
+                                 double* r_out, hipStream_t stream);
+
+/*
+ * Device. Node offsets of the candidate trees (same sizes as d2sd_tree_plan,
+ * computed on the device): node_indptr[0] = 0, node_indptr[b+1] =
+ * node_indptr[b] + B + sum_{k < K[b]} (B - p[b, k]), with K and p clamped the
+ * way d2sd_tree_build clamps them (K to [0, min(Kmax, B-1)], p to [1, B-1]).
+ * Unlike d2sd_tree_plan it does not validate p (distinctness is the caller's
+ * contract, as for d2sd_tree_build). node_indptr: device int32 [batch+1].
+ * Callers that size buffers on the host use the bound
+ * batch * (B + Kmax (B-1) - Kmax (Kmax-1) / 2) for node_indptr[batch].
+ */
+d2sd_status d2sd_tree_indptr(int batch, int B, int Kmax, const int* K, const int* p, int* node_indptr,
+                             hipStream_t stream);
+
 /* ----------------------------------------------- cascade verify attention -- */
 
 /*

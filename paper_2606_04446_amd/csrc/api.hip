@@ -231,6 +231,25 @@ d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int*
                     "tree_build launch");
 }
 
+d2sd_status d2sd_select_reanchor(int batch, int B, int Kmax, const float* conf, const int* K, int* p_out,
+                                 double* r_out, hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (B < 2 || B > D2SD_MAX_B) return fail(D2SD_ERR_INVALID_ARG, "B = %d outside [2, %d]", B, D2SD_MAX_B);
+  if (Kmax < 1) return fail(D2SD_ERR_INVALID_ARG, "Kmax must be >= 1 (got %d)", Kmax);
+  if (!conf || !K || !p_out) return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  return hip_status(d2sd::launch_select_reanchor(batch, B, Kmax, conf, K, p_out, r_out, stream),
+                    "select_reanchor launch");
+}
+
+d2sd_status d2sd_tree_indptr(int batch, int B, int Kmax, const int* K, const int* p, int* node_indptr,
+                             hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (B < 2 || B > D2SD_MAX_B) return fail(D2SD_ERR_INVALID_ARG, "B = %d outside [2, %d]", B, D2SD_MAX_B);
+  if (Kmax < 0) return fail(D2SD_ERR_INVALID_ARG, "Kmax must be >= 0");
+  if (!K || (Kmax > 0 && !p) || !node_indptr) return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  return hip_status(d2sd::launch_tree_indptr(batch, B, Kmax, K, p, node_indptr, stream), "tree_indptr launch");
+}
+
 d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split) {
   d2sd_status s = validate_attn(args, false);
   if (s) return s;

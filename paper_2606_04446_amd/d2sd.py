@@ -72,6 +72,8 @@ _mask_words = _sig("d2sd_mask_words", _c_int, _c_int)
 _tree_plan = _sig("d2sd_tree_plan", _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_int_p)
 _tree_build = _sig("d2sd_tree_build", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_int,
                    _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_select = _sig("d2sd_select_reanchor", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_indptr = _sig("d2sd_tree_indptr", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _ws_size = _sig("d2sd_cascade_workspace_size", _c_int, ctypes.POINTER(AttnArgs), ctypes.POINTER(_c_size))
 _kv_split = _sig("d2sd_cascade_kv_split", _c_int, ctypes.POINTER(AttnArgs), _c_int_p)
 _cascade = _sig("d2sd_cascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr, _c_size, _c_ptr)
@@ -176,6 +178,36 @@ def tree_build(B: int, K, p, node_indptr, total_nodes: int, mask_words_: int, ou
                        _dev(anc_mask, "anc_mask", i32), _dev(path_leaf, "path_leaf", i32), _stream(stream)),
            "d2sd_tree_build")
     return dict(parent=parent, depth=depth, path_id=path_id, anc_mask=anc_mask, path_leaf=path_leaf)
+
+
+def select_reanchor(B: int, conf, K, Kmax: int, p_out=None, r_out=None, want_r: bool = False, stream=None):
+    """Device re-anchor selection (Eq. 4-5). conf: float32 [batch, B-1] device
+    tensor (conf[b, k-1] = c_k), K: int32 [batch]. Returns (p int32 [batch,
+    Kmax], r float64 [batch, B-1] or None)."""
+    import torch
+    batch = K.numel()
+    dev = K.device
+    if conf.shape != (batch, B - 1):
+        raise ValueError(f"conf must have shape ({batch}, {B - 1}), got {tuple(conf.shape)}")
+    p = p_out if p_out is not None else torch.empty((batch, Kmax), dtype=torch.int32, device=dev)
+    r = r_out if r_out is not None else (torch.empty((batch, B - 1), dtype=torch.float64, device=dev)
+                                         if want_r else None)
+    _check(_select(batch, B, Kmax, _dev(conf, "conf", torch.float32), _dev(K, "K", torch.int32),
+                   _dev(p, "p_out", torch.int32), _dev(r, "r_out", torch.float64), _stream(stream)),
+           "d2sd_select_reanchor")
+    return p, r
+
+
+def tree_indptr(B: int, K, p, out=None, stream=None):
+    """Device node offsets (int32 [batch+1]) of the trees of K [batch] and p [batch, Kmax]."""
+    import torch
+    batch = K.numel()
+    kmax = p.shape[1] if p.dim() == 2 else 0
+    ip = out if out is not None else torch.empty(batch + 1, dtype=torch.int32, device=K.device)
+    i32 = torch.int32
+    _check(_indptr(batch, B, kmax, _dev(K, "K", i32), _dev(p, "p", i32) if kmax else None,
+                   _dev(ip, "node_indptr", i32), _stream(stream)), "d2sd_tree_indptr")
+    return ip
 
 
 # -------------------------------------------------------------- attention --

@@ -14,6 +14,7 @@ dim 128). Draw order within a seed, fixed so that a seed names one workload:
   numpy stream 0: context lengths -> branch re-anchor positions -> page
                   permutation
   numpy stream 1: target argmax tokens -> agreement flags -> replacement tokens
+  numpy stream 2: first-drafter confidences (device re-anchor selection input)
   torch generator (seed): Q -> K cache -> V cache -> K tree -> V tree
 """
 
@@ -157,6 +158,15 @@ def custom_layout(B: int, p_rows: Sequence[Sequence[int]], ctx_len: Sequence[int
                 B=B, K=int(K.max(initial=0)), p_rule="explicit", permute_pages=permute_pages)
     table, npages = pages_for(ctx, PAGE, permute_pages, _rng(seed, 0))
     return Layout(spec, seed, K, p, ctx, table, npages)
+
+
+def draw_confidences(layout: "Layout") -> np.ndarray:
+    """First-drafter confidences c_1..c_{B-1} per request, Beta(5, 2), float32
+    [batch, B-1] (numpy stream 2 of the layout seed); input of the device
+    re-anchor selection."""
+    spec = layout.spec
+    rng = _rng(layout.seed, 2)
+    return rng.beta(5.0, 2.0, size=(layout.batch, spec.B - 1)).astype(np.float32)
 
 
 def draw_tokens(layout: Layout, node_indptr: np.ndarray, parent: np.ndarray,

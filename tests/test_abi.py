@@ -89,6 +89,24 @@ def test_tree_build_and_accept_validation():
     assert lib.d2sd_merge_state(4, 128, f, None, f, f, f, f, None) == d2sd.ERR_INVALID_ARG
 
 
+def test_select_reanchor_and_indptr_validation():
+    f = FAKE
+    sel = d2sd._select
+    assert sel(0, 16, 4, f, f, f, None, None) == d2sd.ERR_INVALID_ARG        # batch
+    assert sel(1, 1, 4, f, f, f, None, None) == d2sd.ERR_INVALID_ARG         # B < 2
+    assert sel(1, 65, 4, f, f, f, None, None) == d2sd.ERR_INVALID_ARG        # B > 64
+    assert sel(1, 16, 0, f, f, f, None, None) == d2sd.ERR_INVALID_ARG        # Kmax
+    assert sel(1, 16, 4, None, f, f, None, None) == d2sd.ERR_INVALID_ARG     # conf
+    assert sel(1, 16, 4, f, f, None, None, None) == d2sd.ERR_INVALID_ARG     # p_out
+    ind = d2sd._indptr
+    assert ind(0, 16, 4, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert ind(1, 65, 4, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert ind(1, 16, -1, f, f, f, None) == d2sd.ERR_INVALID_ARG
+    assert ind(1, 16, 4, f, None, f, None) == d2sd.ERR_INVALID_ARG
+    assert ind(1, 16, 4, f, f, None, None) == d2sd.ERR_INVALID_ARG
+    assert "NULL" in d2sd.last_error()
+
+
 def good_args(**kw):
     a = d2sd.AttnArgs()
     a.batch, a.num_qo_heads, a.num_kv_heads, a.head_dim, a.page_size = 32, 32, 8, 128, 16
