@@ -288,6 +288,41 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     res["device_reanchor_us"] = round(e0.elapsed_time(e1) * 1e3 / args.steps, 2)
+
+    # Commit of the accepted paths into the paged cache (the step after the
+    # path): pages for every position below C + B are appended to the pool.
+    acc_c = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax)
+    C = layout.ctx_len.astype(np.int64)
+    have = (C + 15) // 16
+    need = (C + B + 15) // 16
+    table2 = np.zeros((layout.batch, int(need.max())), np.int32)
+    table2[:, :layout.page_table.shape[1]] = layout.page_table
+    nxt = x["k_cache"].shape[0]
+    for b_ in range(layout.batch):
+        for j in range(int(have[b_]), int(need[b_])):
+            table2[b_, j] = nxt
+            nxt += 1
+    grow = nxt - x["k_cache"].shape[0]
+    kc2 = torch.cat([x["k_cache"], torch.zeros((grow,) + tuple(x["k_cache"].shape[1:]), dtype=x["k_cache"].dtype, device=dev)])
+    vc2 = torch.cat([x["v_cache"], torch.zeros((grow,) + tuple(x["v_cache"].shape[1:]), dtype=x["v_cache"].dtype, device=dev)])
+    d_t2 = t(table2)
+    ctx2 = d_ctx.clone()
+    commit = lambda: d2sd.commit_accepted_kv(B, d_ip, total, acc_c["path_nodes"], acc_c["accept_len"], x["k_tree"],
+                                             x["v_tree"], d_t2, ctx2, kc2, vc2, max_ctx_len=max_ctx)
+    for _ in range(3):
+        commit()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        commit()                      # context lengths are clamped to max_ctx: same work every call
+    e1.record()
+    torch.cuda.synchronize()
+    commit_s = e0.elapsed_time(e1) / 1e3 / args.steps
+    n_tok = int((acc_c["accept_len"].cpu().numpy().astype(np.int64) + 1).sum())
+    commit_bytes = 2 * 2 * n_tok * Hkv * D * esz          # K and V rows, read and written
+    res["commit"] = {"us": round(commit_s * 1e6, 2), "tokens": n_tok,
+                     "gbps": round(commit_bytes / commit_s / 1e9, 1)}
+    del kc2, vc2
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(x, layout, node_indptr, parent_host, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -13,6 +13,9 @@
  *                                 states merged by log-sum-exp
  *   d2sd_merge_state      device  the log-sum-exp merge of two attention states
  *   d2sd_accept_path      device  greedy longest-accepted-path selection + bonus
+ *   d2sd_select_reanchor  device  re-anchor positions from drafter confidences (Eq. 4-5)
+ *   d2sd_tree_indptr      device  node offsets of the candidate trees
+ *   d2sd_commit_accepted_kv device accepted path's K/V appended to the paged cache
  *   d2sd_noncascade_verify_attention
  *                         device  same attention, context re-read per tree node
  *                                 (comparison baseline)
@@ -299,6 +302,41 @@ d2sd_status d2sd_accept_path(int batch, int B, const int* node_indptr, int total
                              const int* draft_tokens, const int* target_argmax, int* accept_len,
                              int* best_path, int* accept_node, int* path_nodes, int* out_tokens,
                              hipStream_t stream);
+
+/* -------------------------------------------------------- commit (cache) -- */
+
+/*
+ * Device. Commits every request's accepted path into the paged KV cache
+ * (sec. 3.3: a decoding cycle consumes the verified cache and the previous
+ * bonus token; the longest accepted prefix is committed and the target's
+ * prediction at the rejection point becomes the next anchor). For request b
+ * with context length C = ctx_len[b] and L = accept_len[b], the K and V rows
+ * of the tree nodes path_nodes[b, 0..L] (the anchor, then the L accepted
+ * drafts) are copied to positions C..C+L of the request's pages, position q
+ * living in page page_table[b, q / page_size] at row q % page_size, and
+ * ctx_len[b] becomes C + L + 1. The bonus token (out_tokens[b, L] of
+ * d2sd_accept_path) is not written: it is the next cycle's anchor and its
+ * K/V is computed as the root of the next tree. Nothing else in the cache
+ * changes.
+ *  node_indptr[batch+1], path_nodes[batch, B], accept_len[batch]: as
+ *      produced by d2sd_tree_plan / d2sd_tree_indptr and d2sd_accept_path.
+ *  k_tree, v_tree [total_nodes, num_kv_heads, head_dim] (dtype): this pass's
+ *      tree-node K/V.
+ *  page_table[batch, max_pages]: must already hold pages for every position
+ *      below ctx_len[b] + B (the caller allocates them); ids are clamped to
+ *      [0, num_pages).
+ *  ctx_len[batch]: in/out (device). Values are clamped to [0, max_ctx_len].
+ *  k_cache, v_cache [num_pages, num_kv_heads, page_size, head_dim]: out.
+ * head_dim = D2SD_HEAD_DIM, page_size = D2SD_PAGE_SIZE, dtype D2SD_F32 or
+ * D2SD_BF16; max_ctx_len + B <= max_pages * page_size. Must not run
+ * concurrently with an attention call reading the same cache or ctx_len.
+ * Errors: INVALID_ARG / UNSUPPORTED before any launch.
+ */
+d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head_dim, int page_size, int dtype,
+                                    int num_pages, int max_pages, int max_ctx_len, const int* node_indptr,
+                                    int total_nodes, const int* path_nodes, const int* accept_len,
+                                    const void* k_tree, const void* v_tree, const int* page_table, int* ctx_len,
+                                    void* k_cache, void* v_cache, hipStream_t stream);
 
 /* ------------------------------------------------------------ profiling -- */
 

@@ -15,6 +15,8 @@ Each function computes the plain definition of its step, slowly and visibly:
              token (sec. 2 "DFlash", sec. 3.3 (iv)), two independent ways
   boundary   rejection-boundary posterior r(i) (Eq. 4) and top-K prefix
              lengths (Eq. 5)
+  commit     the accepted path's K/V appended to the paged context (sec. 3.3:
+             each cycle consumes the verified cache and the bonus anchor)
 
 Readings of points the paper leaves open are listed with each function.
 """

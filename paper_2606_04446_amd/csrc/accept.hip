@@ -9,7 +9,7 @@
 // length and the chosen node come from one max-reduction over the key
 // (depth, -index), which implements "deepest accepted node, lowest canonical
 // index on ties".
-#include "common.h"
+#include "launchers.h"
 
 namespace d2sd {
 

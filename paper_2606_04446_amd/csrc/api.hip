@@ -7,7 +7,7 @@
 #include <string>
 #include <vector>
 
-#include "common.h"
+#include "launchers.h"
 
 namespace {
 
@@ -248,6 +248,33 @@ d2sd_status d2sd_tree_indptr(int batch, int B, int Kmax, const int* K, const int
   if (Kmax < 0) return fail(D2SD_ERR_INVALID_ARG, "Kmax must be >= 0");
   if (!K || (Kmax > 0 && !p) || !node_indptr) return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
   return hip_status(d2sd::launch_tree_indptr(batch, B, Kmax, K, p, node_indptr, stream), "tree_indptr launch");
+}
+
+d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head_dim, int page_size, int dtype,
+                                    int num_pages, int max_pages, int max_ctx_len, const int* node_indptr,
+                                    int total_nodes, const int* path_nodes, const int* accept_len,
+                                    const void* k_tree, const void* v_tree, const int* page_table, int* ctx_len,
+                                    void* k_cache, void* v_cache, hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (B < 2 || B > D2SD_MAX_B) return fail(D2SD_ERR_INVALID_ARG, "B = %d outside [2, %d]", B, D2SD_MAX_B);
+  if (num_kv_heads < 1) return fail(D2SD_ERR_INVALID_ARG, "num_kv_heads must be >= 1");
+  if (head_dim != D2SD_HEAD_DIM) return fail(D2SD_ERR_UNSUPPORTED, "head_dim %d != %d", head_dim, D2SD_HEAD_DIM);
+  if (page_size != D2SD_PAGE_SIZE)
+    return fail(D2SD_ERR_UNSUPPORTED, "page_size %d != %d", page_size, D2SD_PAGE_SIZE);
+  if (dtype != D2SD_F32 && dtype != D2SD_BF16) return fail(D2SD_ERR_INVALID_ARG, "dtype %d unknown", dtype);
+  if (num_pages < 1 || max_pages < 1) return fail(D2SD_ERR_INVALID_ARG, "num_pages and max_pages must be >= 1");
+  if (total_nodes < 0 || max_ctx_len < 0) return fail(D2SD_ERR_INVALID_ARG, "negative size");
+  if ((long long)max_ctx_len + B > (long long)max_pages * page_size)
+    return fail(D2SD_ERR_INVALID_ARG, "max_ctx_len + B = %lld exceeds max_pages * page_size = %lld",
+                (long long)max_ctx_len + B, (long long)max_pages * page_size);
+  if (!node_indptr || !path_nodes || !accept_len || !k_tree || !v_tree || !page_table || !ctx_len || !k_cache ||
+      !v_cache)
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  const int row_bytes = head_dim * (dtype == D2SD_BF16 ? 2 : 4);
+  return hip_status(d2sd::launch_commit(batch, B, num_kv_heads, row_bytes, num_pages, max_pages, max_ctx_len,
+                                        node_indptr, total_nodes, path_nodes, accept_len, k_tree, v_tree,
+                                        page_table, ctx_len, k_cache, v_cache, stream),
+                    "commit launch");
 }
 
 d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split) {

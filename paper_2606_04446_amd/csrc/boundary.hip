@@ -9,7 +9,7 @@
 // no contraction), so the selection is reproducible bit for bit. The K largest
 // r(i) are kept, equal values going to the smaller i; prefix length i becomes
 // the re-anchor block position p = i + 1.
-#include "common.h"
+#include "launchers.h"
 
 namespace d2sd {
 

@@ -26,24 +26,6 @@ __device__ __forceinline__ uint32_t range_bits(int lo, int hi, int w) {
   return ones << a;
 }
 
-// Launchers implemented in the .hip files; the C ABI in api.hip validates first.
-hipError_t launch_tree_build(int batch, int B, int Kmax, const int* K, const int* p,
-                             const int* node_indptr, int total_nodes, int mask_words, int* parent,
-                             int* depth, int* path_id, uint32_t* anc_mask, int* path_leaf,
-                             hipStream_t stream);
-
-hipError_t launch_select_reanchor(int batch, int B, int Kmax, const float* conf, const int* K, int* p_out,
-                                  double* r_out, hipStream_t stream);
-
-hipError_t launch_tree_indptr(int batch, int B, int Kmax, const int* K, const int* p, int* node_indptr,
-                              hipStream_t stream);
-
-hipError_t launch_accept_path(int batch, int B, const int* node_indptr, int total_nodes,
-                              const int* parent, const int* depth, const int* path_id,
-                              const int* draft, const int* argmax, int* accept_len, int* best_path,
-                              int* accept_node, int* path_nodes, int* out_tokens,
-                              hipStream_t stream);
-
 // Resolved plan of one verify-attention call (host side).
 struct AttnPlan {
   int G;             // query heads per KV head

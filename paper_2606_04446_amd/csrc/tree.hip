@@ -7,7 +7,7 @@
 // prefix {0 .. p_k - 1} plus the branch run {off_k .. n}. A main node j sees
 // {0 .. j}. Every mask word is therefore the union of two bit ranges, which is
 // computed directly instead of walking parent pointers.
-#include "common.h"
+#include "launchers.h"
 
 namespace d2sd {
 

@@ -74,6 +74,8 @@ _tree_build = _sig("d2sd_tree_build", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c
                    _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _select = _sig("d2sd_select_reanchor", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _indptr = _sig("d2sd_tree_indptr", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_commit = _sig("d2sd_commit_accepted_kv", _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+               _c_int, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _ws_size = _sig("d2sd_cascade_workspace_size", _c_int, ctypes.POINTER(AttnArgs), ctypes.POINTER(_c_size))
 _kv_split = _sig("d2sd_cascade_kv_split", _c_int, ctypes.POINTER(AttnArgs), _c_int_p)
 _cascade = _sig("d2sd_cascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr, _c_size, _c_ptr)
@@ -208,6 +210,24 @@ def tree_indptr(B: int, K, p, out=None, stream=None):
     _check(_indptr(batch, B, kmax, _dev(K, "K", i32), _dev(p, "p", i32) if kmax else None,
                    _dev(ip, "node_indptr", i32), _stream(stream)), "d2sd_tree_indptr")
     return ip
+
+
+def commit_accepted_kv(B: int, node_indptr, total_nodes: int, path_nodes, accept_len, k_tree, v_tree,
+                       page_table, ctx_len, k_cache, v_cache, max_ctx_len: int, stream=None):
+    """Append every request's accepted path K/V to its pages (in place on
+    k_cache / v_cache) and advance ctx_len (in place). Shapes as in the header."""
+    import torch
+    code = {torch.float32: F32, torch.bfloat16: BF16}.get(k_cache.dtype)
+    if code is None or k_tree.dtype != k_cache.dtype:
+        raise ValueError("k/v cache and tree must share dtype float32 or bfloat16")
+    i32 = torch.int32
+    batch = ctx_len.numel()
+    _check(_commit(batch, B, k_cache.shape[1], k_cache.shape[3], k_cache.shape[2], code, k_cache.shape[0],
+                   page_table.shape[1], max_ctx_len, _dev(node_indptr, "node_indptr", i32), total_nodes,
+                   _dev(path_nodes, "path_nodes", i32), _dev(accept_len, "accept_len", i32),
+                   _dev(k_tree, "k_tree"), _dev(v_tree, "v_tree"), _dev(page_table, "page_table", i32),
+                   _dev(ctx_len, "ctx_len", i32), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+                   _stream(stream)), "d2sd_commit_accepted_kv")
 
 
 # -------------------------------------------------------------- attention --

@@ -107,6 +107,23 @@ def test_select_reanchor_and_indptr_validation():
     assert "NULL" in d2sd.last_error()
 
 
+def test_commit_validation():
+    f = FAKE
+    c = d2sd._commit
+    ok = dict(batch=1, B=16, hkv=8, D=128, P=16, dt=d2sd.BF16, npages=64, maxp=64, maxc=1000)
+    def call(**kw):
+        a = {**ok, **kw}
+        return c(a["batch"], a["B"], a["hkv"], a["D"], a["P"], a["dt"], a["npages"], a["maxp"], a["maxc"],
+                 f, 10, f, f, f, f, f, f, f, f, None)
+    assert call(batch=0) == d2sd.ERR_INVALID_ARG
+    assert call(B=1) == d2sd.ERR_INVALID_ARG
+    assert call(D=64) == d2sd.ERR_UNSUPPORTED
+    assert call(P=32) == d2sd.ERR_UNSUPPORTED
+    assert call(dt=5) == d2sd.ERR_INVALID_ARG
+    assert call(maxc=64 * 16 - 15) == d2sd.ERR_INVALID_ARG     # positions up to C + B must have pages
+    assert c(1, 16, 8, 128, 16, d2sd.BF16, 64, 64, 100, f, 10, f, f, f, f, f, None, f, f, None) == d2sd.ERR_INVALID_ARG
+
+
 def good_args(**kw):
     a = d2sd.AttnArgs()
     a.batch, a.num_qo_heads, a.num_kv_heads, a.head_dim, a.page_size = 32, 32, 8, 128, 16
