@@ -42,6 +42,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--noncascade", action="store_true", help="also time the non-cascade baseline kernel")
+    ap.add_argument("--tree", choices=["canonical", "third_level", "resample"], default="canonical",
+                    help="tree shape: the canonical chain-plus-branches tree (default), the third-level cascade "
+                         "(a sub-branch inside every branch) or K+1 resampled chains, the latter two built from "
+                         "parent arrays")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy three times (HBM counter calibration)")
     return ap.parse_args()
@@ -91,13 +95,13 @@ def measured_traffic(config: int, kv_split: int, resolved_split: int):
     return r.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float):
+def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float, parents=None):
     """The oracle, as it stands, on whole requests until the time budget is spent."""
     import torch
     from threadpoolctl import threadpool_info
 
     from oracle.attention import gather_context, request_attention
-    from oracle.tree import build_tree
+    from oracle.tree import build_tree, tree_from_parents
 
     done_nodes, done_req = 0, 0
     t_total = 0.0
@@ -112,7 +116,8 @@ def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float):
         kt = x["k_tree"][s:e].float().cpu().numpy()
         vt = x["v_tree"][s:e].float().cpu().numpy()
         t0 = time.perf_counter()
-        tree = build_tree(layout.spec.B, layout.p[b, :layout.K[b]])
+        tree = (build_tree(layout.spec.B, layout.p[b, :layout.K[b]]) if parents is None
+                else tree_from_parents(parents[b], layout.spec.B))
         kcb, vcb = gather_context(kc, vc, np.arange(npg), C, 16)
         request_attention(q.astype(np.float64), kcb, vcb, kt.astype(np.float64), vt.astype(np.float64), tree)
         t_total += time.perf_counter() - t0
@@ -151,7 +156,16 @@ def main():
     layout = wl.draw_layout(args.config)
     spec = layout.spec
     B = spec.B
-    node_indptr, W = d2sd.tree_plan(B, layout.K, layout.p)
+    parents = None
+    if args.tree == "canonical":
+        node_indptr, W = d2sd.tree_plan(B, layout.K, layout.p)
+    else:
+        q_sub = wl.draw_sub_branch_positions(layout)
+        parents = [wl.parent_array(B, layout.p[b, :layout.K[b]], q_sub[b, :layout.K[b]])
+                   if args.tree == "third_level" else wl.parent_array(B, [], chains=int(layout.K[b]) + 1)
+                   for b in range(layout.batch)]
+        node_indptr = np.concatenate([[0], np.cumsum([len(pa) for pa in parents])]).astype(np.int32)
+        W = (int(np.diff(node_indptr).max()) + 31) // 32
     total = int(node_indptr[-1])
     max_nodes = int(np.diff(node_indptr).max())
     max_ctx = int(layout.ctx_len.max())
@@ -160,7 +174,12 @@ def main():
     d_ctx, d_pt = t(layout.ctx_len), t(layout.page_table)
     x = wl.draw_tensors(layout, total, device=dev)
 
-    tree = d2sd.tree_build(B, d_K, d_p, d_ip, total, W)
+    if parents is None:
+        build = lambda out=None: d2sd.tree_build(B, d_K, d_p, d_ip, total, W, out=out)
+    else:
+        d_par = t(np.concatenate(parents))
+        build = lambda out=None: d2sd.tree_from_parents(d_ip, total, max_nodes, d_par, W, out=out)
+    tree = build()
     torch.cuda.synchronize()
     parent_host = tree["parent"].cpu().numpy()
     draft, argmax = wl.draw_tokens(layout, node_indptr, parent_host)
@@ -176,7 +195,7 @@ def main():
     acc = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax)
 
     def step():
-        d2sd.tree_build(B, d_K, d_p, d_ip, total, W, out=tree)
+        build(out=tree)
         d2sd.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"],
                                       d_ip, tree["anc_mask"], total_nodes=total, max_nodes=max_nodes,
                                       max_ctx_len=max_ctx, kv_split=args.kv_split, out=out, lse=lse,
@@ -215,7 +234,7 @@ def main():
     tflops = flops / t_s / 1e12
     t_hbm = prefix_bytes / (HBM_PEAK_GBPS * 1e9)
     t_mfma = flops / (MFMA_PEAK_TFLOPS[spec.dtype] * 1e12)
-    traffic = measured_traffic(args.config, args.kv_split, kv_split)
+    traffic = measured_traffic(args.config, args.kv_split, kv_split) if args.tree == "canonical" else None
     if t_mfma > t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_PEAK_TFLOPS[spec.dtype],
                 "unit": "TFLOP/s", "frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4), "traffic": traffic}
@@ -239,7 +258,7 @@ def main():
         "config": {"workload": spec.name, "batch": layout.batch,
                    "ctx_len": [int(ctx.min()), int(ctx.max())], "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "block": B, "branches": spec.K, "tree_nodes": total,
-                   "page_size": spec.page_size, "kv_split": kv_split},
+                   "page_size": spec.page_size, "kv_split": kv_split, "tree": args.tree},
         "roofline": roof,
         "prefix_kv_gbps": round(gbps, 1),
         "prefix_kv_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
@@ -324,7 +343,7 @@ def main():
                      "gbps": round(commit_bytes / commit_s / 1e9, 1)}
     del kc2, vc2
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(x, layout, node_indptr, parent_host, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(x, layout, node_indptr, parent_host, args.cpu_seconds, parents)
     print(json.dumps(res), flush=True)
 
 

@@ -13,6 +13,7 @@
  *                                 states merged by log-sum-exp
  *   d2sd_merge_state      device  the log-sum-exp merge of two attention states
  *   d2sd_accept_path      device  greedy longest-accepted-path selection + bonus
+ *   d2sd_tree_from_parents device general trees (third-level cascade, resampling)
  *   d2sd_select_reanchor  device  re-anchor positions from drafter confidences (Eq. 4-5)
  *   d2sd_tree_indptr      device  node offsets of the candidate trees
  *   d2sd_commit_accepted_kv device accepted path's K/V appended to the paged cache
@@ -139,6 +140,29 @@ d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int*
                             const int* node_indptr, int total_nodes, int mask_words,
                             int* parent, int* depth, int* path_id, uint32_t* anc_mask,
                             int* path_leaf, hipStream_t stream);
+
+/*
+ * Device. Trees given as parent arrays, for candidate sets that are not the
+ * canonical chain-plus-branches tree: the third-level cascade (sec. 4.3:
+ * every branch gets a sub-branch re-anchored inside its tail, up to 2K+1
+ * candidates sharing prefixes) and independent resampling (K+1 chains under
+ * the anchor). Request b's nodes are node_indptr[b] .. node_indptr[b+1]-1,
+ * in topological order: local node 0 is the anchor (parent -1) and every
+ * other node's parent precedes it; a parent outside [0, n) makes node n a
+ * root of its own. Outputs (device, caller-allocated), same meaning as for
+ * d2sd_tree_build:
+ *   depth[ΣN]     edges to the root
+ *   path_id[ΣN]   number of path-starting nodes m in 1..n (m starts a path
+ *                 when its parent is not m - 1); equals the branch number on
+ *                 a canonical tree
+ *   anc_mask[ΣN, mask_words] ancestor-or-self bits over local indices
+ * The outputs feed d2sd_cascade_verify_attention and d2sd_accept_path
+ * unchanged (the accept path needs depths <= B - 1). 1 <= max_nodes <= 2080
+ * bounds every request's node count; mask_words * 32 >= max_nodes.
+ */
+d2sd_status d2sd_tree_from_parents(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                   int mask_words, const int* parent, int* depth, int* path_id,
+                                   uint32_t* anc_mask, hipStream_t stream);
 
 /*
  * Device. Re-anchor selection from the first drafter's confidences (sec. 3.1

@@ -125,3 +125,76 @@ def build_tree(B: int, p) -> Tree:
             c = parent[c]
         ancestors.append(s)
     return Tree(B, ps, position, path, parent, ancestors)
+
+
+def tree_from_parents(parent, B: int | None = None) -> Tree:
+    """Tree of one request from an arbitrary parent array: the general trees
+    of the third-level cascade (sec. 4.3, up to 2K+1 candidates sharing
+    prefixes) and of independent resampling (K+1 chains under the anchor).
+
+    Readings (generalising the canonical tree):
+      * node 0 is the anchor (root, parent -1); every other node's parent
+        precedes it (0 <= parent[n] < n), i.e. nodes are topologically ordered;
+      * depth = number of edges to the root;
+      * node n starts a new path when its parent is not node n - 1, and
+        path[n] counts the path-starting nodes among 1..n (on a canonical tree
+        this is the branch number); p lists the depth at which each extra path
+        starts (the re-anchor position, for a canonical tree);
+      * ancestor-or-self sets by walking parents, as for the canonical tree.
+    B defaults to the largest depth + 1."""
+    parent = [int(x) for x in parent]
+    if not parent or parent[0] != -1:
+        raise ValueError("node 0 must be the root (parent -1)")
+    for n in range(1, len(parent)):
+        if not 0 <= parent[n] < n:
+            raise ValueError(f"node {n}: parent {parent[n]} must lie in [0, {n})")
+    position, ancestors = [], []
+    for n in range(len(parent)):
+        s, c = set(), n
+        while c != -1:
+            s.add(c)
+            c = parent[c]
+        ancestors.append(s)
+        position.append(len(s) - 1)
+    path, starts = [], 0
+    p = []
+    for n in range(len(parent)):
+        if n > 0 and parent[n] != n - 1:
+            starts += 1
+            p.append(position[n])
+        path.append(starts)
+    if B is None:
+        B = max(position) + 1
+    return Tree(B, p, position, path, parent, ancestors)
+
+
+def third_level_parents(B: int, p, q) -> list:
+    """Parent array of the third-level cascade tree (sec. 4.3): the canonical
+    tree of (B, p) plus, for branch k (ascending p), a sub-branch re-anchored
+    at position q[k] (p[k] < q[k] <= B-1) inside that branch's tail: it keeps
+    the branch up to q[k] - 1 and owns positions q[k]..B-1. Sub-branches come
+    after all branches, in branch order."""
+    t = build_tree(B, p)
+    parent = list(t.parent)
+    for k, pk in enumerate(t.p, start=1):
+        qk = int(q[k - 1])
+        if not pk < qk <= B - 1:
+            raise ValueError(f"sub-branch position {qk} outside ({pk}, {B - 1}]")
+        # branch node holding position qk - 1 (the branch itself when qk - 1 >= pk)
+        prev = [n for n in range(t.N) if t.path[n] == k and t.position[n] == qk - 1][0]
+        for _ in range(qk, B):
+            parent.append(prev)
+            prev = len(parent) - 1
+    return parent
+
+
+def resample_parents(B: int, chains: int) -> list:
+    """Parent array of `chains` independent draft chains of B-1 tokens under
+    one anchor (the naive resampling baseline of sec. 1 / sec. 4.3)."""
+    parent = [-1]
+    for _ in range(chains):
+        prev = 0
+        for _ in range(1, B):
+            parent.append(prev)
+            prev = len(parent) - 1
+    return parent

@@ -66,6 +66,10 @@ void timing_begin(hipEvent_t* e0, hipEvent_t* e1) {
   g_timing_pending.emplace_back(*e0, *e1);
 }
 
+// Largest tree any entry point accepts: the canonical tree of B = D2SD_MAX_B
+// with every re-anchor position (the accept kernel stages one tree in LDS).
+constexpr int kMaxTreeNodes = D2SD_MAX_B + D2SD_MAX_B * (D2SD_MAX_B - 1) / 2;
+
 int mask_words_for(int B) {
   if (B < 2 || B > D2SD_MAX_B) return 0;
   return (B + B * (B - 1) / 2 + 31) / 32;
@@ -229,6 +233,22 @@ d2sd_status d2sd_tree_build(int batch, int B, int Kmax, const int* K, const int*
   return hip_status(d2sd::launch_tree_build(batch, B, Kmax, K, p, node_indptr, total_nodes, mask_words,
                                             parent, depth, path_id, anc_mask, path_leaf, stream),
                     "tree_build launch");
+}
+
+d2sd_status d2sd_tree_from_parents(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                   int mask_words, const int* parent, int* depth, int* path_id,
+                                   uint32_t* anc_mask, hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (total_nodes < 0) return fail(D2SD_ERR_INVALID_ARG, "total_nodes must be >= 0");
+  if (max_nodes < 1 || max_nodes > kMaxTreeNodes)
+    return fail(D2SD_ERR_INVALID_ARG, "max_nodes %d outside [1, %d]", max_nodes, kMaxTreeNodes);
+  if ((long long)mask_words * 32 < max_nodes)
+    return fail(D2SD_ERR_INVALID_ARG, "mask_words %d too small for max_nodes %d", mask_words, max_nodes);
+  if (!node_indptr || !parent || !depth || !path_id || !anc_mask)
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  return hip_status(d2sd::launch_tree_from_parents(batch, node_indptr, total_nodes, max_nodes, mask_words, parent,
+                                                   depth, path_id, anc_mask, stream),
+                    "tree_from_parents launch");
 }
 
 d2sd_status d2sd_select_reanchor(int batch, int B, int Kmax, const float* conf, const int* K, int* p_out,

@@ -12,6 +12,10 @@ hipError_t launch_tree_build(int batch, int B, int Kmax, const int* K, const int
                              int* depth, int* path_id, uint32_t* anc_mask, int* path_leaf,
                              hipStream_t stream);
 
+hipError_t launch_tree_from_parents(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                    int mask_words, const int* parent, int* depth, int* path_id,
+                                    uint32_t* anc_mask, hipStream_t stream);
+
 hipError_t launch_select_reanchor(int batch, int B, int Kmax, const float* conf, const int* K, int* p_out,
                                   double* r_out, hipStream_t stream);
 

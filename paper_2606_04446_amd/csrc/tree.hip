@@ -78,7 +78,64 @@ __global__ __launch_bounds__(kTreeThreads) void tree_build_kernel(
   }
 }
 
+// Trees given as parent arrays (node 0 the root, parent[n] < n): the
+// third-level cascade and resampled chains. Node n walks its parent links,
+// setting one mask bit per ancestor-or-self and counting the depth; a parent
+// outside [0, n) makes n a root of its own. path_id[n] counts the nodes m in
+// 1..n whose parent is not m - 1 (path starts), by a chunked block scan.
+__global__ __launch_bounds__(kTreeThreads) void tree_from_parents_kernel(
+    const int* __restrict__ node_indptr, int total_nodes, int max_nodes, int mask_words,
+    const int* __restrict__ parent, int* __restrict__ depth, int* __restrict__ path_id,
+    uint32_t* __restrict__ anc_mask) {
+  __shared__ int s_scan[kTreeThreads];
+  __shared__ int s_carry;
+  const int b = blockIdx.x;
+  const int t = threadIdx.x;
+  const int base = clampi(node_indptr[b], 0, total_nodes);
+  const int Nb = clampi(node_indptr[b + 1] - base, 0, min(max_nodes, total_nodes - base));
+  auto par_of = [&](int n) {
+    const int q = parent[base + n];
+    return (q >= 0 && q < n) ? q : -1;
+  };
+  for (int n = t; n < Nb; n += kTreeThreads) {
+    uint32_t* row = anc_mask + (size_t)(base + n) * mask_words;
+    for (int w = 0; w < mask_words; ++w) row[w] = 0u;
+    int d = -1;
+    for (int a = n; a >= 0; a = par_of(a)) {
+      row[a >> 5] |= 1u << (a & 31);
+      ++d;
+    }
+    depth[base + n] = d;
+  }
+  if (t == 0) s_carry = 0;
+  __syncthreads();
+  for (int n0 = 0; n0 < Nb; n0 += kTreeThreads) {
+    const int n = n0 + t;
+    s_scan[t] = (n > 0 && n < Nb && parent[base + n] != n - 1) ? 1 : 0;
+    __syncthreads();
+    for (int dd = 1; dd < kTreeThreads; dd <<= 1) {
+      const int v = t >= dd ? s_scan[t - dd] : 0;
+      __syncthreads();
+      s_scan[t] += v;
+      __syncthreads();
+    }
+    const int carry = s_carry;
+    if (n < Nb) path_id[base + n] = carry + s_scan[t];
+    __syncthreads();
+    if (t == kTreeThreads - 1) s_carry = carry + s_scan[t];
+    __syncthreads();
+  }
+}
+
 }  // namespace
+
+hipError_t launch_tree_from_parents(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                    int mask_words, const int* parent, int* depth, int* path_id,
+                                    uint32_t* anc_mask, hipStream_t stream) {
+  hipLaunchKernelGGL(tree_from_parents_kernel, dim3(batch), dim3(kTreeThreads), 0, stream, node_indptr,
+                     total_nodes, max_nodes, mask_words, parent, depth, path_id, anc_mask);
+  return hipGetLastError();
+}
 
 hipError_t launch_tree_build(int batch, int B, int Kmax, const int* K, const int* p,
                              const int* node_indptr, int total_nodes, int mask_words, int* parent,

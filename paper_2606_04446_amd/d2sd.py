@@ -72,6 +72,8 @@ _mask_words = _sig("d2sd_mask_words", _c_int, _c_int)
 _tree_plan = _sig("d2sd_tree_plan", _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_int_p)
 _tree_build = _sig("d2sd_tree_build", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_int,
                    _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_from_parents = _sig("d2sd_tree_from_parents", _c_int, _c_int, _c_ptr, _c_int, _c_int, _c_int, _c_ptr, _c_ptr,
+                     _c_ptr, _c_ptr, _c_ptr)
 _select = _sig("d2sd_select_reanchor", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _indptr = _sig("d2sd_tree_indptr", _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _commit = _sig("d2sd_commit_accepted_kv", _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
@@ -180,6 +182,25 @@ def tree_build(B: int, K, p, node_indptr, total_nodes: int, mask_words_: int, ou
                        _dev(anc_mask, "anc_mask", i32), _dev(path_leaf, "path_leaf", i32), _stream(stream)),
            "d2sd_tree_build")
     return dict(parent=parent, depth=depth, path_id=path_id, anc_mask=anc_mask, path_leaf=path_leaf)
+
+
+def tree_from_parents(node_indptr, total_nodes: int, max_nodes: int, parent, mask_words_: int | None = None,
+                      out: dict | None = None, stream=None) -> dict:
+    """Device tree arrays from a parent array (int32 [ΣN], local indices).
+    Returns dict(parent, depth, path_id, anc_mask) shaped as tree_build's outputs."""
+    import torch
+    batch = node_indptr.numel() - 1
+    W = mask_words_ if mask_words_ is not None else (max_nodes + 31) // 32
+    dev = parent.device
+    o = out or {}
+    depth = o["depth"] if "depth" in o else torch.empty(total_nodes, dtype=torch.int32, device=dev)
+    path_id = o["path_id"] if "path_id" in o else torch.empty(total_nodes, dtype=torch.int32, device=dev)
+    anc_mask = o["anc_mask"] if "anc_mask" in o else torch.empty((total_nodes, W), dtype=torch.int32, device=dev)
+    i32 = torch.int32
+    _check(_from_parents(batch, _dev(node_indptr, "node_indptr", i32), total_nodes, max_nodes, W,
+                         _dev(parent, "parent", i32), _dev(depth, "depth", i32), _dev(path_id, "path_id", i32),
+                         _dev(anc_mask, "anc_mask", i32), _stream(stream)), "d2sd_tree_from_parents")
+    return dict(parent=parent, depth=depth, path_id=path_id, anc_mask=anc_mask)
 
 
 def select_reanchor(B: int, conf, K, Kmax: int, p_out=None, r_out=None, want_r: bool = False, stream=None):

@@ -15,6 +15,7 @@ dim 128). Draw order within a seed, fixed so that a seed names one workload:
                   permutation
   numpy stream 1: target argmax tokens -> agreement flags -> replacement tokens
   numpy stream 2: first-drafter confidences (device re-anchor selection input)
+  numpy stream 3: sub-branch positions (third-level tree shape)
   torch generator (seed): Q -> K cache -> V cache -> K tree -> V tree
 """
 
@@ -167,6 +168,60 @@ def draw_confidences(layout: "Layout") -> np.ndarray:
     spec = layout.spec
     rng = _rng(layout.seed, 2)
     return rng.beta(5.0, 2.0, size=(layout.batch, spec.B - 1)).astype(np.float32)
+
+
+def draw_sub_branch_positions(layout: "Layout") -> np.ndarray:
+    """Re-anchor position q_k of the sub-branch inside branch k's tail for the
+    third-level tree shape: uniform in (p_k, B-1], or 0 (no sub-branch) when
+    p_k = B-1. int32 [batch, Kmax] (numpy stream 3 of the layout seed)."""
+    B = layout.spec.B
+    rng = _rng(layout.seed, 3)
+    q = np.zeros_like(layout.p)
+    for b in range(layout.batch):
+        for k in range(int(layout.K[b])):
+            pk = int(layout.p[b, k])
+            q[b, k] = int(rng.integers(pk + 1, B)) if pk < B - 1 else 0
+    return q
+
+
+def parent_array(B: int, p_row: Sequence[int], q_row: Optional[Sequence[int]] = None,
+                 chains: int = 0) -> np.ndarray:
+    """Parent array (local indices, node 0 the anchor) of one request's tree,
+    as input for the parent-array tree builder:
+      chains > 0  `chains` independent chains of B-1 drafts under the anchor;
+      otherwise   the first-draft chain, one branch per re-anchor position p
+                  (ascending) hanging under the chain node at p - 1, and, when
+                  q_row is given, per branch a sub-branch hanging under the
+                  branch node at q - 1 (q > p; 0 = none), after all branches."""
+    par = [-1]
+    if chains > 0:
+        for _ in range(chains):
+            prev = 0
+            for _ in range(B - 1):
+                par.append(prev)
+                prev = len(par) - 1
+        return np.asarray(par, np.int32)
+    for j in range(1, B):
+        par.append(j - 1)
+    order = sorted(range(len(p_row)), key=lambda k: p_row[k])
+    at = {}                                     # (branch, position) -> node
+    for k in order:
+        pk = int(p_row[k])
+        prev = pk - 1
+        for pos in range(pk, B):
+            par.append(prev)
+            prev = len(par) - 1
+            at[(k, pos)] = prev
+    if q_row is not None:
+        for k in order:
+            qk = int(q_row[k])
+            if qk <= 0:
+                continue
+            prev = at[(k, qk - 1)] if qk - 1 >= int(p_row[k]) else qk - 1
+            for _ in range(qk, B):
+                par.append(prev)
+                prev = len(par) - 1
+    return np.asarray(par, np.int32)
 
 
 def draw_tokens(layout: Layout, node_indptr: np.ndarray, parent: np.ndarray,
