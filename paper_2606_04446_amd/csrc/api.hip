@@ -78,7 +78,8 @@ int mask_words_for(int B) {
 // ---- verify-attention planning ----
 
 constexpr int kNumCUs = 256;
-constexpr int kMinSplit = 256;
+constexpr int kMinSplit = 256;      // bf16: shorter splits cost more in partial states than they gain
+constexpr int kMinSplitF32 = 64;    // fp32: a split is compute-bound (fp32 MFMA), parallelism pays
 constexpr int kMaxSplit = 32768;   // the bf16 kernel stages a split's page ids in LDS
 
 d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
@@ -128,22 +129,24 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
 }
 
 // Context tokens per split. Automatic choice: enough (request, KV head, row
-// group, split) work items for about two rounds of resident workgroups (two
+// group, split) work items for about two rounds of resident workgroups (three
 // per CU for the 4-wave bf16 kernel, one otherwise), but no split shorter
-// than kMinSplit tokens (the partial state of a split costs as many bytes as
-// ~M/2 keys of K/V, M = rows sharing it).
+// than the dtype's minimum (the partial state of a split costs as many bytes
+// as ~M/2 keys of K/V, M = rows sharing it; fp32 splits are compute-bound and
+// can be shorter).
 int choose_split(const d2sd_attn_args* a, int G) {
   if (a->kv_split > 0) return a->kv_split;
   const int ctx = a->max_ctx_len;
-  if (ctx <= kMinSplit) return ((max(ctx, 1) + 63) / 64) * 64;
+  const int min_split = a->dtype == D2SD_F32 ? kMinSplitF32 : kMinSplit;
+  if (ctx <= min_split) return ((max(ctx, 1) + 63) / 64) * 64;
   const double avg_nodes = (double)a->total_nodes / a->batch;
   const int avg_tiles = (int)ceil(avg_nodes * G / d2sd::kRowsPerTile);
   const int tiles_per_group = d2sd::group_rows(a->dtype) / d2sd::kRowsPerTile;
   const int avg_groups = max(1, (avg_tiles + tiles_per_group - 1) / tiles_per_group);
   const long long base = (long long)a->batch * a->num_kv_heads * avg_groups;
-  const int resident = kNumCUs * (a->dtype == D2SD_BF16 && d2sd::kBf16Waves == 4 ? 2 : 1);
+  const int resident = kNumCUs * (a->dtype == D2SD_BF16 && d2sd::kBf16Waves == 4 ? 3 : 1);
   int splits = (int)((2ll * resident + base - 1) / base);
-  splits = max(max(1, (ctx + kMaxSplit - 1) / kMaxSplit), min(splits, ctx / kMinSplit));
+  splits = max(max(1, (ctx + kMaxSplit - 1) / kMaxSplit), min(splits, ctx / min_split));
   const int per = (ctx + splits - 1) / splits;
   return ((per + 63) / 64) * 64;
 }

@@ -539,11 +539,13 @@ __global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 kernel (the hot path): 8 waves, two per SIMD, one 32-query column tile
-// per wave. K/V tiles of 64 keys are copied global -> LDS by the LDS DMA path
-// (global_load_lds_dwordx4: no staging registers, no VALU) into a four-stage
-// ring, so three tiles are in flight while one is consumed. Both tiles keep
-// the natural [key][dim] layout with 16-byte chunks XOR-swizzled by row:
+// bf16 kernel (the hot path): workgroups of 4 waves, one 32-query column tile
+// per wave, three workgroups per CU (40 KB of LDS and 163 VGPRs each), so
+// every SIMD interleaves three independent waves. K/V tiles of 32 keys are
+// copied global -> LDS by the LDS DMA path (global_load_lds_dwordx4: no
+// staging registers, no VALU) into a two-stage ring: the copy of tile j+1 is
+// in flight while tile j is consumed. Both tiles keep the natural [key][dim]
+// layout with 16-byte chunks XOR-swizzled by row:
 //   K: chunk c of row r sits at c ^ (r & 15)   (b128 A-operand reads of 16
 //      consecutive keys hit 16 distinct bank groups)
 //   V: chunk c of row r sits at c ^ 4(r & 3)   (transposing b64 reads)
@@ -555,10 +557,11 @@ namespace bf {
 constexpr int WAVES = kBf16Waves;        // waves per workgroup, one 32-query tile each
 constexpr int THREADS = WAVES * kWave;
 constexpr int MAX_SPLIT_PAGES = 2048;    // page ids of one context split staged in LDS
-constexpr int KT = 64;                   // keys per tile
+constexpr int KT = 32;                   // keys per tile (a 40 KB workgroup: three per CU)
+constexpr int NKB = KT / 32;             // 32-key MFMA blocks per tile
 constexpr int ROW_BYTES = kD * 2;        // 256 B per key row
 constexpr int TILE_BYTES = KT * ROW_BYTES;  // 16 KB for K (and for V)
-constexpr int NSTAGE = WAVES == 8 ? 4 : 2;  // LDS ring depth (two workgroups per CU fit at 2)
+constexpr int NSTAGE = WAVES == 8 ? 4 : 2;  // LDS ring depth
 constexpr int BLOCKS = KT / 4;           // 1 KB (four-row) DMA blocks per K or V tile
 constexpr int WAVE_BLOCKS = BLOCKS / WAVES;   // K (and V) blocks copied by each wave
 constexpr int DMA_PER_TILE = 2 * WAVE_BLOCKS; // DMA instructions per wave per tile
@@ -719,26 +722,26 @@ __device__ __forceinline__ ReadLane read_lane(int lane) {
   return rl;
 }
 
-// S^T of one query tile for a 64-key tile (two 32-key blocks).
+// S^T of one query tile for a key tile (NKB blocks of 32 keys).
 __device__ __forceinline__ void qk_tile(const char* sK, const ReadLane& rl, const bf16x8 (&q)[8],
-                                        f32x16 (&s)[2]) {
-  s[0] = f32x16{};
-  s[1] = f32x16{};
+                                        f32x16 (&s)[bf::NKB]) {
+#pragma unroll
+  for (int kb = 0; kb < bf::NKB; ++kb) s[kb] = f32x16{};
 #pragma unroll
   for (int st = 0; st < 8; ++st) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < bf::NKB; ++kb) {
       const bf16x8 a = __builtin_bit_cast(bf16x8, lds_b128(sK, rl.k[st] + kb * 32 * bf::ROW_BYTES));
       s[kb] = mfma(a, q[st], s[kb]);
     }
   }
 }
 
-// O^T += V^T P^T over a 64-key tile (4 k-steps of 16 keys).
-__device__ __forceinline__ void pv_tile(const char* sV, const ReadLane& rl, const bf16x8 (&pf)[4],
+// O^T += V^T P^T over a key tile (2 NKB k-steps of 16 keys).
+__device__ __forceinline__ void pv_tile(const char* sV, const ReadLane& rl, const bf16x8 (&pf)[2 * bf::NKB],
                                         f32x16 (&o)[4]) {
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
+  for (int ks = 0; ks < 2 * bf::NKB; ++ks) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       const s16x4 lo = lds_tr16(sV, rl.v[dt] + (ks * 16) * bf::ROW_BYTES);
@@ -759,25 +762,25 @@ __device__ __forceinline__ float xhalf_max(float x) {
 // 32 kb + (i/4)*8 + hf*4 + i%4 of the tile. `vis` holds the visible keys of
 // the tile; after shifting out the lane half's offset every slot tests a
 // fixed bit.
-__device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int nvalid, uint64_t vis, int hf) {
+__device__ __forceinline__ void mask_tile(f32x16 (&s)[bf::NKB], int nvalid, uint64_t vis, int hf) {
   const uint64_t in_range = nvalid >= 64 ? ~0ull : ((1ull << max(nvalid, 0)) - 1ull);
   const uint64_t m = (vis & in_range) >> (hf * 4);
-  const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+  const uint32_t w[2] = {(uint32_t)m, (uint32_t)(m >> 32)};
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int bit = (i >> 2) * 8 + (i & 3);
-    s[0][i] = ((lo >> bit) & 1u) ? s[0][i] : -INFINITY;
-    s[1][i] = ((hi >> bit) & 1u) ? s[1][i] : -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < bf::NKB; ++kb) s[kb][i] = ((w[kb] >> bit) & 1u) ? s[kb][i] : -INFINITY;
   }
 }
 
-// Online softmax of one query tile over 64 keys: updates the running max /
+// Online softmax of one query tile over a key tile: updates the running max /
 // sum / output scale and leaves bf16 probabilities in B-operand order.
-__device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], float& m_run, float& l_run, f32x16 (&o)[4],
-                                             bf16x8 (&pf)[4], float c2) {
+__device__ __forceinline__ void softmax_tile(f32x16 (&s)[bf::NKB], float& m_run, float& l_run, f32x16 (&o)[4],
+                                             bf16x8 (&pf)[2 * bf::NKB], float c2) {
   float mx = -INFINITY;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < bf::NKB; ++kb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
   mx = xhalf_max(mx);
@@ -795,7 +798,7 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], float& m_run, float
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float la = 0.0f, lb = 0.0f;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int kb = 0; kb < bf::NKB; ++kb) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       bf16x8 v;
@@ -821,7 +824,7 @@ __device__ __forceinline__ uint64_t tree_bits(const Params& p, int node_base, in
   return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
-__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(bf::WAVES == 4 ? 2 : 1)))
+__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void cascade_bf16_kernel(Params p) {
   constexpr int GROUP_ROWS = bf::WAVES * kRowsPerTile;
   // LDS ring stages as separate arrays (keeps DMA targets and reads apart)
@@ -933,7 +936,7 @@ void cascade_bf16_kernel(Params p) {
     if (!active) return;
     const TileSrc ts = src(jt);
     const int nvalid = ts.key_end - ts.key0;
-    f32x16 s[2];
+    f32x16 s[bf::NKB];
     qk_tile(cK, rl, q, s);
     if (ts.tree || nvalid < bf::KT) {
       uint64_t vis = ~0ull;
@@ -942,7 +945,7 @@ void cascade_bf16_kernel(Params p) {
       }
       mask_tile(s, nvalid, vis, hf);
     }
-    bf16x8 pf[4];
+    bf16x8 pf[2 * bf::NKB];
     softmax_tile(s, m_run, l_run, o, pf, p.c2);
     pv_tile(cV, rl, pf, o);
   };

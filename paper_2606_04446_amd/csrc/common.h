@@ -48,8 +48,8 @@ hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const fl
                               hipStream_t stream);
 
 // Waves (one 32-query column tile each) per workgroup of the bf16 kernel.
-// Four waves let two workgroups share a CU, so one computes while the other
-// waits on its barrier or its copies.
+// Four-wave workgroups let three workgroups share a CU, so each SIMD runs
+// three independent waves that hide each other's barrier and copy waits.
 #ifndef D2SD_BF16_WAVES
 #define D2SD_BF16_WAVES 4
 #endif
