@@ -46,6 +46,9 @@ def parse():
                     help="tree shape: the canonical chain-plus-branches tree (default), the third-level cascade "
                          "(a sub-branch inside every branch) or K+1 resampled chains, the latter two built from "
                          "parent arrays")
+    ap.add_argument("--graph", action="store_true",
+                    help="also capture the step in a HIP graph and take `value` from graph replays "
+                         "(measured no faster than eager launches: the step is not launch-bound)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy three times (HBM counter calibration)")
     return ap.parse_args()
@@ -216,9 +219,33 @@ def main():
     ev1.record()
     torch.cuda.synchronize()
     d2sd.kernel_timing_enable(False)
-    step_ms = ev0.elapsed_time(ev1) / args.steps
+    step_ms_eager = ev0.elapsed_time(ev1) / args.steps
     launches, kern_ms_total = d2sd.kernel_timing_collect()
     kern_ms = kern_ms_total / max(launches, 1)
+
+    # The same step captured once in a HIP graph and replayed: the four
+    # launches of a step then cost one graph launch (the step allocates
+    # nothing and issues no memset, so it can be captured as it is).
+    step_ms = step_ms_eager
+    if args.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(args.steps):
+            graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        step_ms = ev0.elapsed_time(ev1) / args.steps
 
     # algorithmic work of one launch of the cascade kernel
     esz = 2 if spec.dtype == "bf16" else 4
@@ -250,6 +277,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(step_ms, 4),
+        "ms_per_step_eager": round(step_ms_eager, 4),
+        "graph": bool(args.graph),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
