@@ -144,7 +144,7 @@ int choose_split(const d2sd_attn_args* a, int G) {
   const int tiles_per_group = d2sd::group_rows(a->dtype) / d2sd::kRowsPerTile;
   const int avg_groups = max(1, (avg_tiles + tiles_per_group - 1) / tiles_per_group);
   const long long base = (long long)a->batch * a->num_kv_heads * avg_groups;
-  const int resident = kNumCUs * (a->dtype == D2SD_BF16 && d2sd::kBf16Waves == 4 ? 3 : 1);
+  const int resident = kNumCUs * (a->dtype == D2SD_BF16 ? 3 : 1);
   int splits = (int)((2ll * resident + base - 1) / base);
   splits = max(max(1, (ctx + kMaxSplit - 1) / kMaxSplit), min(splits, ctx / min_split));
   const int per = (ctx + splits - 1) / splits;

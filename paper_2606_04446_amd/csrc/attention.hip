@@ -63,19 +63,9 @@ struct Params {
   float c2;  // sm_scale * log2(e)
 };
 
-// Element-type specific tiling.
+// Tiling of the generic kernel (instantiated for fp32; bf16 has its own kernel).
 template <typename T>
 struct Tile;
-
-template <>
-struct Tile<__bf16> {
-  static constexpr int KT = 64;         // keys per tile
-  static constexpr int WT = 2;          // 32-query column tiles per wave
-  static constexpr int KS = 136;        // K row stride (elements): 272 B, conflict-free b128 reads
-  static constexpr int VS = 72;         // V^T row stride (elements): 144 B
-  static constexpr int K_ELEMS = KT * KS;
-  static constexpr int V_ELEMS = kD * VS;
-};
 
 template <>
 struct Tile<float> {
@@ -115,66 +105,6 @@ __device__ __forceinline__ const T* key_row(const Params& p, const T* base_cache
 }
 
 // ---- staging of one K/V tile: global -> registers -> LDS ------------------
-
-struct StageBf16 {
-  uint4 k[4];
-  uint4 v[4];
-};
-
-// bf16: K chunk i of thread t covers key 16i + t/16, dims (t%16)*8..+8, so the
-// 256 threads read one 4 KB page slab per i. V: thread t covers dims
-// (t/16)*8..+8 of the 4 keys 4*(t%16)..+3 (transposed when stored).
-__device__ __forceinline__ void load_tile(const Params& p, StageBf16& st, bool tree, int b, int h,
-                                          int node_base, int key0, int key_end) {
-  const __bf16* kc = static_cast<const __bf16*>(p.k_cache);
-  const __bf16* vc = static_cast<const __bf16*>(p.v_cache);
-  const __bf16* kt = static_cast<const __bf16*>(p.k_tree);
-  const __bf16* vt = static_cast<const __bf16*>(p.v_tree);
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int key = 16 * i + (t >> 4);
-    const __bf16* r = key_row(p, kc, kt, tree, b, h, node_base, key0 + key, key_end);
-    st.k[i] = r ? *reinterpret_cast<const uint4*>(r + (t & 15) * 8) : zero4();
-  }
-  const int oct = t >> 4;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int key = 4 * (t & 15) + e;
-    const __bf16* r = key_row(p, vc, vt, tree, b, h, node_base, key0 + key, key_end);
-    st.v[e] = r ? *reinterpret_cast<const uint4*>(r + oct * 8) : zero4();
-  }
-}
-
-__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
-__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
-
-__device__ __forceinline__ void store_tile(const StageBf16& st, __bf16* sK, __bf16* sV) {
-  using C = Tile<__bf16>;
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int key = 16 * i + (t >> 4);
-    *reinterpret_cast<uint4*>(sK + key * C::KS + (t & 15) * 8) = st.k[i];
-  }
-  // V^T: the 4 keys of this thread land in 4 adjacent columns of the permuted
-  // key order (within each 16-key group: 0-3, 8-11 | 4-7, 12-15), which is the
-  // order the PV B operand takes straight from the S^T accumulator.
-  const int kq = t & 15;
-  const int col = (kq >> 2) * 16 + (kq & 1) * 8 + ((kq >> 1) & 1) * 4;
-  const int dim0 = (t >> 4) * 8;
-  const uint32_t w0[4] = {st.v[0].x, st.v[0].y, st.v[0].z, st.v[0].w};
-  const uint32_t w1[4] = {st.v[1].x, st.v[1].y, st.v[1].z, st.v[1].w};
-  const uint32_t w2[4] = {st.v[2].x, st.v[2].y, st.v[2].z, st.v[2].w};
-  const uint32_t w3[4] = {st.v[3].x, st.v[3].y, st.v[3].z, st.v[3].w};
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    uint2 even = make_uint2(lo_pair(w0[j], w1[j]), lo_pair(w2[j], w3[j]));
-    uint2 odd = make_uint2(hi_pair(w0[j], w1[j]), hi_pair(w2[j], w3[j]));
-    *reinterpret_cast<uint2*>(sV + (dim0 + 2 * j) * C::VS + col) = even;
-    *reinterpret_cast<uint2*>(sV + (dim0 + 2 * j + 1) * C::VS + col) = odd;
-  }
-}
 
 struct StageF32 {
   uint4 k[4];
@@ -217,11 +147,6 @@ __device__ __forceinline__ void store_tile(const StageF32& st, float* sK, float*
 template <typename T>
 struct Frag;
 template <>
-struct Frag<__bf16> {
-  using Q = bf16x8;
-  static constexpr int QN = 8;   // k-steps over the head dim (16 dims each)
-};
-template <>
 struct Frag<float> {
   using Q = float;
   static constexpr int QN = 64;  // k-steps over the head dim (2 dims each)
@@ -247,19 +172,6 @@ __device__ __forceinline__ void load_q(const Params& p, float (&qf)[64], const f
 }
 
 // S^T block (32 keys starting at key row kb of the LDS tile) for one query tile.
-__device__ __forceinline__ f32x16 score_block(const __bf16* sK, int kb, const bf16x8 (&qf)[8],
-                                              int lane) {
-  using C = Tile<__bf16>;
-  f32x16 acc = {};
-  const int hf = lane >> 5;
-  const __bf16* base = sK + (kb + (lane & 31)) * C::KS + hf * 64;
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + s * 8));
-    acc = mfma(a, qf[s], acc);
-  }
-  return acc;
-}
 __device__ __forceinline__ f32x16 score_block(const float* sK, int kb, const float (&qf)[64],
                                               int lane) {
   using C = Tile<float>;
@@ -272,26 +184,6 @@ __device__ __forceinline__ f32x16 score_block(const float* sK, int kb, const flo
 }
 
 // O^T (4 dim tiles of 32) += V^T P^T for one 32-key block of the tile.
-// bf16: the block's probabilities p[0..15] become two 16-key k-steps.
-__device__ __forceinline__ void pv_block(const __bf16* sV, int kb, const f32x16& pr,
-                                         f32x16 (&o)[4], int lane) {
-  using C = Tile<__bf16>;
-  const int hf = lane >> 5;
-  bf16x8 b0, b1;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    b0[j] = (__bf16)pr[j];
-    b1[j] = (__bf16)pr[8 + j];
-  }
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) {
-    const __bf16* base = sV + (dt * 32 + (lane & 31)) * C::VS + kb + hf * 8;
-    bf16x8 a0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base));
-    bf16x8 a1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + 16));
-    o[dt] = mfma(a0, b0, o[dt]);
-    o[dt] = mfma(a1, b1, o[dt]);
-  }
-}
 // fp32: accumulator slot i of lane half hf is key kb + (i/4)*8 + hf*4 + i%4.
 __device__ __forceinline__ void pv_block(const float* sV, int kb, const f32x16& pr, f32x16 (&o)[4],
                                          int lane) {
@@ -307,10 +199,6 @@ __device__ __forceinline__ void pv_block(const float* sV, int kb, const f32x16& 
 
 template <typename T>
 struct Stage;
-template <>
-struct Stage<__bf16> {
-  using type = StageBf16;
-};
 template <>
 struct Stage<float> {
   using type = StageF32;
@@ -561,10 +449,8 @@ constexpr int KT = 32;                   // keys per tile (a 40 KB workgroup: th
 constexpr int NKB = KT / 32;             // 32-key MFMA blocks per tile
 constexpr int ROW_BYTES = kD * 2;        // 256 B per key row
 constexpr int TILE_BYTES = KT * ROW_BYTES;  // 16 KB for K (and for V)
-constexpr int NSTAGE = WAVES == 8 ? 4 : 2;  // LDS ring depth
 constexpr int BLOCKS = KT / 4;           // 1 KB (four-row) DMA blocks per K or V tile
 constexpr int WAVE_BLOCKS = BLOCKS / WAVES;   // K (and V) blocks copied by each wave
-constexpr int DMA_PER_TILE = 2 * WAVE_BLOCKS; // DMA instructions per wave per tile
 constexpr float kRescaleLog2 = 8.0f;     // move the running max when it grows by > 2^8
 }  // namespace bf
 
@@ -609,14 +495,6 @@ __device__ __forceinline__ void sync_keep() {
   __builtin_amdgcn_s_waitcnt((N & 15) | 0x0070 | ((N >> 4) << 14));
   asm volatile("s_barrier" ::: "memory");
 }
-// Wait until the oldest tile's copy is complete while `later_tiles` younger
-// tiles (at most NSTAGE - 2) stay in flight, then barrier.
-__device__ __forceinline__ void sync_tiles_in_flight(int later_tiles) {
-  if (bf::NSTAGE > 3 && later_tiles >= 2) sync_keep<2 * bf::DMA_PER_TILE>();
-  else if (bf::NSTAGE > 2 && later_tiles >= 1) sync_keep<bf::DMA_PER_TILE>();
-  else sync_keep<0>();
-}
-
 struct TileSrc {
   bool tree;
   int key0;
@@ -827,13 +705,9 @@ __device__ __forceinline__ uint64_t tree_bits(const Params& p, int node_base, in
 __global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void cascade_bf16_kernel(Params p) {
   constexpr int GROUP_ROWS = bf::WAVES * kRowsPerTile;
-  // LDS ring stages as separate arrays (keeps DMA targets and reads apart)
+  // the two stages of the K/V ring
   __shared__ __attribute__((aligned(1024))) char sk0[bf::TILE_BYTES], sv0[bf::TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char sk1[bf::TILE_BYTES], sv1[bf::TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char sk2[bf::NSTAGE > 2 ? bf::TILE_BYTES : 16];
-  __shared__ __attribute__((aligned(1024))) char sv2[bf::NSTAGE > 2 ? bf::TILE_BYTES : 16];
-  __shared__ __attribute__((aligned(1024))) char sk3[bf::NSTAGE > 3 ? bf::TILE_BYTES : 16];
-  __shared__ __attribute__((aligned(1024))) char sv3[bf::NSTAGE > 3 ? bf::TILE_BYTES : 16];
   __shared__ __attribute__((aligned(16))) int s_pid[bf::MAX_SPLIT_PAGES + 4];
 
   // ---- work item (XCD-aware: consecutive items share an XCD and its L2) ----
@@ -922,17 +796,14 @@ void cascade_bf16_kernel(Params p) {
       dma_tile(p, ts, h, node_base, s_pid, c0, dl, const_cast<char*>(sK), const_cast<char*>(sV));
   };
 
-  // prologue: tiles 0 .. NSTAGE-2 in flight
-  constexpr int AHEAD = bf::NSTAGE - 1;
+  // prologue: tile 0 in flight
   if (n_tiles > 0) copy_tile(0, sk0, sv0);
-  if (AHEAD > 1 && n_tiles > 1) copy_tile(1, sk1, sv1);
-  if (AHEAD > 2 && n_tiles > 2) copy_tile(2, sk2, sv2);
 
-  // One tile: wait for its copy (keeping later tiles in flight), queue the
-  // tile NSTAGE-1 ahead into the stage freed by the previous tile, compute.
+  // One tile: wait for its copy and for every wave to be done with the
+  // previous tile, queue the next tile into the stage that one used, compute.
   auto step = [&](int jt, const char* cK, const char* cV, char* nK, char* nV) {
-    sync_tiles_in_flight(min(AHEAD - 1, n_tiles - 1 - jt));
-    if (jt + AHEAD < n_tiles) copy_tile(jt + AHEAD, nK, nV);
+    sync_keep<0>();
+    if (jt + 1 < n_tiles) copy_tile(jt + 1, nK, nV);
     if (!active) return;
     const TileSrc ts = src(jt);
     const int nvalid = ts.key_end - ts.key0;
@@ -949,18 +820,9 @@ void cascade_bf16_kernel(Params p) {
     softmax_tile(s, m_run, l_run, o, pf, p.c2);
     pv_tile(cV, rl, pf, o);
   };
-  if constexpr (bf::NSTAGE == 4) {
-    for (int jt = 0; jt < n_tiles; jt += 4) {
-      step(jt, sk0, sv0, sk3, sv3);
-      if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
-      if (jt + 2 < n_tiles) step(jt + 2, sk2, sv2, sk1, sv1);
-      if (jt + 3 < n_tiles) step(jt + 3, sk3, sv3, sk2, sv2);
-    }
-  } else {
-    for (int jt = 0; jt < n_tiles; jt += 2) {
-      step(jt, sk0, sv0, sk1, sv1);
-      if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
-    }
+  for (int jt = 0; jt < n_tiles; jt += 2) {
+    step(jt, sk0, sv0, sk1, sv1);
+    if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
   }
 
   // ---- epilogue: finalise (single split) or write the split partial ----

@@ -50,11 +50,7 @@ hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const fl
 // Waves (one 32-query column tile each) per workgroup of the bf16 kernel.
 // Four-wave workgroups let three workgroups share a CU, so each SIMD runs
 // three independent waves that hide each other's barrier and copy waits.
-#ifndef D2SD_BF16_WAVES
-#define D2SD_BF16_WAVES 4
-#endif
-constexpr int kBf16Waves = D2SD_BF16_WAVES;
-static_assert(kBf16Waves == 4 || kBf16Waves == 8, "bf16 workgroup size");
+constexpr int kBf16Waves = 4;
 
 // Rows (queries) per MFMA column tile, and rows per workgroup row group of
 // the cascade kernel (one tile per wave: kBf16Waves for bf16, 4 for fp32);
