@@ -17,6 +17,9 @@ Each function computes the plain definition of its step, slowly and visibly:
              lengths (Eq. 5)
   commit     the accepted path's K/V appended to the paged context (sec. 3.3:
              each cycle consumes the verified cache and the bonus anchor)
+  sampling   verification at T > 0 (Tables 3-4 report T = 1; the tree rule is
+             a reading): one target draw per distinct context by inversion,
+             then the greedy longest-path rule on the drawn tokens
 
 Readings of points the paper leaves open are listed with each function.
 """
