@@ -3,6 +3,8 @@ attention -> accept path, on a seeded synthetic batch resident in HBM.
 
     python bench.py [--steps K] [--warmup W] [--config 4] [--kv-split S]
                     [--cpu-seconds 15] [--no-cpu-baseline] [--noncascade]
+                    [--tree canonical|third_level|resample] [--graph]
+                    [--temperature 1.0] [--sample-vocab 32000]
     python bench.py --copy-probe       (HBM counter calibration copy)
 
 Prints one JSON line. value = verified tree tokens per second of the whole
@@ -46,6 +48,10 @@ def parse():
                     help="tree shape: the canonical chain-plus-branches tree (default), the third-level cascade "
                          "(a sub-branch inside every branch) or K+1 resampled chains, the latter two built from "
                          "parent arrays")
+    ap.add_argument("--temperature", type=float, default=1.0,
+                    help="temperature of the separately timed sampling-verification draws")
+    ap.add_argument("--sample-vocab", type=int, default=32000,
+                    help="vocabulary of the target logits for the sampling draws")
     ap.add_argument("--graph", action="store_true",
                     help="also capture the step in a HIP graph and take `value` from graph replays "
                          "(measured no faster than eager launches: the step is not launch-bound)")
@@ -371,6 +377,33 @@ def main():
     res["commit"] = {"us": round(commit_s * 1e6, 2), "tokens": n_tok,
                      "gbps": round(commit_bytes / commit_s / 1e9, 1)}
     del kc2, vc2
+
+    # Sampling verification (T > 0): a target draw at every node from its
+    # logits row (bf16 [nodes, vocab]), one draw per distinct context, then the
+    # accept path on the drawn tokens; timed on its own (not in `value`).
+    Vs = args.sample_vocab
+    logits = wl.draw_logits(layout, argmax, vocab=Vs, device=dev, dtype="bf16")
+    d_u = t(wl.draw_uniforms(layout, total))
+    toks = torch.empty(total, dtype=torch.int32, device=dev)
+    draw = lambda: d2sd.sample_targets(d_ip, total, max_nodes, tree["parent"], d_draft, logits, args.temperature,
+                                       d_u, out=toks)
+    for _ in range(3):
+        draw()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        draw()
+    e1.record()
+    torch.cuda.synchronize()
+    draw_s = e0.elapsed_time(e1) / 1e3 / args.steps
+    acc_t = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, toks)
+    draw_bytes = total * Vs * 2                            # every node streams one logits row once
+    draw_gbps = draw_bytes / draw_s / 1e9
+    res["sampling"] = {"temperature": args.temperature, "vocab": Vs, "rows": total, "us": round(draw_s * 1e6, 2),
+                       "gbps": round(draw_gbps, 1), "hbm_frac": round(draw_gbps / HBM_PEAK_GBPS, 4),
+                       "mean_accept_len": round(float(acc_t["accept_len"].float().mean()), 3),
+                       "greedy_mean_accept_len": round(float(acc["accept_len"].float().mean()), 3)}
+    del logits
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(x, layout, node_indptr, parent_host, args.cpu_seconds, parents)
     print(json.dumps(res), flush=True)

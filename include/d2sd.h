@@ -13,6 +13,8 @@
  *                                 states merged by log-sum-exp
  *   d2sd_merge_state      device  the log-sum-exp merge of two attention states
  *   d2sd_accept_path      device  greedy longest-accepted-path selection + bonus
+ *   d2sd_sample_targets   device  target token per node from logits: draw at
+ *                                 T > 0 (one per distinct context), argmax at T = 0
  *   d2sd_tree_from_parents device general trees (third-level cascade, resampling)
  *   d2sd_select_reanchor  device  re-anchor positions from drafter confidences (Eq. 4-5)
  *   d2sd_tree_indptr      device  node offsets of the candidate trees
@@ -78,6 +80,7 @@ typedef int d2sd_status;
 #define D2SD_MAX_B 64        /* block length; a request's mask row fits 2080 nodes */
 #define D2SD_HEAD_DIM 128
 #define D2SD_PAGE_SIZE 16
+#define D2SD_MAX_VOCAB 1048576 /* logits per row for d2sd_sample_targets */
 
 /* Static string for a status code; never NULL. */
 const char* d2sd_status_string(d2sd_status s);
@@ -326,6 +329,47 @@ d2sd_status d2sd_accept_path(int batch, int B, const int* node_indptr, int total
                              const int* draft_tokens, const int* target_argmax, int* accept_len,
                              int* best_path, int* accept_node, int* path_nodes, int* out_tokens,
                              hipStream_t stream);
+
+/* --------------------------------------------------- sampling verification -- */
+
+/*
+ * Device. Target tokens at every tree node for verification at temperature T
+ * (Tables 3-4 report T = 1 next to greedy decoding; the paper states no tree
+ * rule for T > 0, so this is the rule taken here). Feed the result to
+ * d2sd_accept_path as target_argmax: the longest-accepted-path selection and
+ * the bonus token are then those of the sampling rule.
+ *  - T > 0: node n's token is drawn from softmax(logits[r] / T) by inversion
+ *    with uniform[r]: the smallest token index j with
+ *      sum_{i <= j} w_i > uniform[r] * sum_i w_i,  w_i = exp((l_i - max l) / T),
+ *    sums in vocabulary order (fp32 weights, fp32 sums). If rounding leaves no
+ *    such j, the last token of positive weight is taken.
+ *  - T = 0: the argmax of logits[r], the lowest index on ties.
+ *  - r is n's representative: the lowest-index node of the same request whose
+ *    root path has the same length and the same draft tokens (the same
+ *    context). Nodes with one context thus share one draw, which keeps the
+ *    emitted tokens distributed as the target's when branches repeat a
+ *    context; a child is then accepted with probability p(its token), the
+ *    rejection-sampling rule for drafted tokens taken as point masses.
+ * A row with no finite logit gives -1. Logits must be finite or -inf (NaN and
+ * +inf give an unspecified token in [-1, vocab)).
+ * Inputs (device): node_indptr[batch+1]; parent[ΣN] (local indices, parents
+ * before children, -1 for the root, as from d2sd_tree_build or
+ * d2sd_tree_from_parents); draft_tokens[ΣN] (the root's entry is not
+ * compared); logits[ΣN, vocab] row-major, dtype D2SD_F32 or D2SD_BF16, the
+ * target's next-token logits after each node, 16-byte aligned; uniform[ΣN]
+ * float32 in [0, 1) (read only for representatives; may be NULL when
+ * temperature == 0).
+ * Outputs (device, caller-allocated): target_tokens[ΣN] int32;
+ * context_rep[ΣN] int32 local representative index (nullable).
+ * 1 <= max_nodes <= 2080 must bound every request's node count; batch *
+ * max_nodes < 2^31; 1 <= vocab <= D2SD_MAX_VOCAB; temperature is 0 or in
+ * [1e-6, 1e6]. total_nodes = node_indptr[batch] (host value) bounds every read.
+ * Root paths longer than 64 nodes leave a node as its own representative.
+ */
+d2sd_status d2sd_sample_targets(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                const int* parent, const int* draft_tokens, int vocab, int dtype,
+                                const void* logits, float temperature, const float* uniform,
+                                int* context_rep, int* target_tokens, hipStream_t stream);
 
 /* -------------------------------------------------------- commit (cache) -- */
 

@@ -68,8 +68,11 @@ def sample_token(logits, T: float, u: float) -> int:
 
     T = 0: argmax, lowest index on ties. T > 0: the smallest j with
     sum_{i <= j} w_i > u * sum_i w_i, where w_i = exp((l_i - max l) / T). If
-    rounding leaves no such j, the last token of positive weight is taken."""
+    rounding leaves no such j, the last token of positive weight is taken.
+    A row with no finite logit defines no distribution and gives -1."""
     x = np.asarray(logits, dtype=np.float64)
+    if not np.isfinite(np.max(x)):
+        return -1
     if T == 0:
         return int(np.argmax(x))               # first maximum
     m = np.max(x)

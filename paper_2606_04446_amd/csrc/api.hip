@@ -385,6 +385,30 @@ d2sd_status d2sd_accept_path(int batch, int B, const int* node_indptr, int total
                     "accept_path launch");
 }
 
+d2sd_status d2sd_sample_targets(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                const int* parent, const int* draft_tokens, int vocab, int dtype,
+                                const void* logits, float temperature, const float* uniform,
+                                int* context_rep, int* target_tokens, hipStream_t stream) {
+  if (batch < 1) return fail(D2SD_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (total_nodes < 0) return fail(D2SD_ERR_INVALID_ARG, "total_nodes must be >= 0");
+  if (max_nodes < 1 || max_nodes > kMaxTreeNodes)
+    return fail(D2SD_ERR_INVALID_ARG, "max_nodes = %d outside [1, %d]", max_nodes, kMaxTreeNodes);
+  if ((long long)batch * max_nodes > 0x7fffffffLL)
+    return fail(D2SD_ERR_INVALID_ARG, "batch * max_nodes = %lld exceeds 2^31 - 1", (long long)batch * max_nodes);
+  if (vocab < 1 || vocab > D2SD_MAX_VOCAB)
+    return fail(D2SD_ERR_INVALID_ARG, "vocab = %d outside [1, %d]", vocab, D2SD_MAX_VOCAB);
+  if (dtype != D2SD_F32 && dtype != D2SD_BF16) return fail(D2SD_ERR_INVALID_ARG, "dtype %d unknown", dtype);
+  if (!(temperature == 0.0f || (temperature >= 1e-6f && temperature <= 1e6f)))
+    return fail(D2SD_ERR_INVALID_ARG, "temperature must be 0 or in [1e-6, 1e6]");
+  if (!node_indptr || !parent || !draft_tokens || !logits || !target_tokens || (temperature != 0.0f && !uniform))
+    return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(logits) % 16 != 0) return fail(D2SD_ERR_INVALID_ARG, "logits not 16-byte aligned");
+  return hip_status(d2sd::launch_sample_targets(batch, node_indptr, total_nodes, max_nodes, parent, draft_tokens,
+                                                vocab, dtype, logits, temperature, uniform, context_rep,
+                                                target_tokens, stream),
+                    "sample_targets launch");
+}
+
 d2sd_status d2sd_kernel_timing_enable(int enable) {
   std::lock_guard<std::mutex> lk(g_timing_mu);
   g_timing_on = enable != 0;

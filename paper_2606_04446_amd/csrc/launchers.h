@@ -33,4 +33,9 @@ hipError_t launch_accept_path(int batch, int B, const int* node_indptr, int tota
                               int* accept_node, int* path_nodes, int* out_tokens,
                               hipStream_t stream);
 
+hipError_t launch_sample_targets(int batch, const int* node_indptr, int total_nodes, int max_nodes,
+                                 const int* parent, const int* draft, int vocab, int dtype, const void* logits,
+                                 float temperature, const float* uniform, int* context_rep, int* tokens,
+                                 hipStream_t stream);
+
 }  // namespace d2sd

@@ -86,6 +86,8 @@ _merge = _sig("d2sd_merge_state", _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr
               _c_ptr)
 _accept = _sig("d2sd_accept_path", _c_int, _c_int, _c_int, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
+_sample = _sig("d2sd_sample_targets", _c_int, _c_int, _c_ptr, _c_int, _c_int, _c_ptr, _c_ptr, _c_int, _c_int, _c_ptr,
+                ctypes.c_float, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _timing_enable = _sig("d2sd_kernel_timing_enable", _c_int, _c_int)
 _timing_collect = _sig("d2sd_kernel_timing_collect", _c_int, _c_int_p, ctypes.POINTER(ctypes.c_double))
 
@@ -379,6 +381,33 @@ def accept_path(B: int, node_indptr, total_nodes: int, parent, depth, path_id, d
                    _dev(res["accept_node"], "accept_node", i32), _dev(res["path_nodes"], "path_nodes", i32),
                    _dev(res["out_tokens"], "out_tokens", i32), _stream(stream)), "d2sd_accept_path")
     return res
+
+
+# -------------------------------------------------- sampling verification --
+
+def sample_targets(node_indptr, total_nodes: int, max_nodes: int, parent, draft_tokens, logits,
+                   temperature: float, uniform=None, want_rep: bool = False, out=None, rep_out=None, stream=None):
+    """Target token at every tree node from its logits row (float32 or
+    bfloat16 [ΣN, vocab]): a draw by inversion with `uniform` (float32 [ΣN])
+    at temperature > 0, the argmax at 0; nodes with one context share the draw
+    of their representative. Returns (tokens int32 [ΣN], reps int32 [ΣN] or None)."""
+    import torch
+    code = {torch.float32: F32, torch.bfloat16: BF16}.get(logits.dtype)
+    if code is None:
+        raise ValueError(f"logits dtype {logits.dtype} unsupported (float32 or bfloat16)")
+    if logits.dim() != 2 or logits.shape[0] < total_nodes:
+        raise ValueError(f"logits must be [>= {total_nodes}, vocab], got {tuple(logits.shape)}")
+    batch = node_indptr.numel() - 1
+    dev = node_indptr.device
+    i32 = torch.int32
+    tokens = out if out is not None else torch.empty(max(total_nodes, 1), dtype=i32, device=dev)
+    reps = rep_out if rep_out is not None else (torch.empty(max(total_nodes, 1), dtype=i32, device=dev)
+                                                if want_rep else None)
+    _check(_sample(batch, _dev(node_indptr, "node_indptr", i32), total_nodes, max_nodes, _dev(parent, "parent", i32),
+                   _dev(draft_tokens, "draft_tokens", i32), logits.shape[1], code, _dev(logits, "logits"),
+                   float(temperature), _dev(uniform, "uniform", torch.float32), _dev(reps, "context_rep", i32),
+                   _dev(tokens, "target_tokens", i32), _stream(stream)), "d2sd_sample_targets")
+    return tokens[:total_nodes], (reps[:total_nodes] if reps is not None else None)
 
 
 # ---------------------------------------------------------------- timing --

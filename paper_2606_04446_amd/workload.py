@@ -16,7 +16,9 @@ dim 128). Draw order within a seed, fixed so that a seed names one workload:
   numpy stream 1: target argmax tokens -> agreement flags -> replacement tokens
   numpy stream 2: first-drafter confidences (device re-anchor selection input)
   numpy stream 3: sub-branch positions (third-level tree shape)
+  numpy stream 4: uniforms of the sampling draws
   torch generator (seed): Q -> K cache -> V cache -> K tree -> V tree
+  torch generator (seed + 2^32): target logits
 """
 
 from __future__ import annotations
@@ -252,6 +254,45 @@ def draw_tokens(layout: Layout, node_indptr: np.ndarray, parent: np.ndarray,
             tgt = argmax[s + par[c]]
             draft[g] = tgt if flags[g] else (tgt + 1 + other[g]) % VOCAB
     return draft.astype(np.int32), argmax.astype(np.int32)
+
+
+def logit_boost(vocab: int, sigma: float, p_top: float) -> float:
+    """Logit added to one token so that it takes about probability p_top at
+    T = 1 against vocab - 1 others with N(0, sigma^2) logits: the others'
+    exp-sum is about vocab * exp(sigma^2 / 2)."""
+    return float(np.log(vocab * np.exp(sigma * sigma / 2.0) * p_top / (1.0 - p_top)))
+
+
+def draw_logits(layout: Layout, preferred: np.ndarray, vocab: int = VOCAB, device="cpu", dtype: str = "bf16",
+                sigma: float = 2.0, p_top: float = 0.7, chunk_rows: int = 1024):
+    """Target next-token logits per tree node, [len(preferred), vocab]: every
+    logit N(0, sigma^2), plus logit_boost(vocab, sigma, p_top) on the node's
+    preferred token (the target argmax drawn by draw_tokens), so that at T = 1
+    the preferred token is drawn with probability about p_top and acceptance
+    resembles the greedy workloads'. Drawn in fp32 from a torch generator
+    seeded with seed + 2^32, rounded to the element type."""
+    import torch
+
+    dt = torch_dtype(dtype)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(layout.seed) + (1 << 32))
+    n = len(preferred)
+    out = torch.empty((n, vocab), dtype=dt, device=device)
+    boost = logit_boost(vocab, sigma, p_top)
+    pref = torch.as_tensor(np.asarray(preferred, np.int64), device=device)
+    for s in range(0, n, chunk_rows):
+        e = min(n, s + chunk_rows)
+        x = torch.randn((e - s, vocab), generator=gen, device=device, dtype=torch.float32) * sigma
+        x[torch.arange(e - s, device=device), pref[s:e]] += boost
+        out[s:e] = x.to(dt)
+    return out
+
+
+def draw_uniforms(layout: Layout, total_nodes: int) -> np.ndarray:
+    """One uniform in [0, 1) per tree node (float32; numpy stream 4), the
+    random input of the sampling draws."""
+    u = _rng(layout.seed, 4).random(total_nodes, dtype=np.float32)
+    return np.minimum(u, np.float32(np.nextafter(np.float32(1.0), np.float32(0.0))))
 
 
 def torch_dtype(name: str):

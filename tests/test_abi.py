@@ -124,6 +124,31 @@ def test_commit_validation():
     assert c(1, 16, 8, 128, 16, d2sd.BF16, 64, 64, 100, f, 10, f, f, f, f, f, None, f, f, None) == d2sd.ERR_INVALID_ARG
 
 
+def test_sample_targets_validation():
+    f = FAKE
+    ok = dict(batch=1, total=10, maxn=10, V=32000, dt=d2sd.BF16, logits=f, T=1.0, u=f)
+
+    def call(**kw):
+        a = {**ok, **kw}
+        return d2sd._sample(a["batch"], f, a["total"], a["maxn"], f, f, a["V"], a["dt"], a["logits"], a["T"],
+                            a["u"], None, f, None)
+    assert call(batch=0) == d2sd.ERR_INVALID_ARG
+    assert call(total=-1) == d2sd.ERR_INVALID_ARG
+    assert call(maxn=0) == d2sd.ERR_INVALID_ARG
+    assert call(maxn=2081) == d2sd.ERR_INVALID_ARG
+    assert call(batch=2 ** 20, maxn=2080) == d2sd.ERR_INVALID_ARG          # grid beyond 2^31 - 1
+    assert call(V=0) == d2sd.ERR_INVALID_ARG
+    assert call(V=(1 << 20) + 1) == d2sd.ERR_INVALID_ARG
+    assert call(dt=7) == d2sd.ERR_INVALID_ARG
+    for T in (-1.0, 1e-7, 2e6, math.inf, math.nan):
+        assert call(T=T) == d2sd.ERR_INVALID_ARG, T
+    assert call(u=None) == d2sd.ERR_INVALID_ARG                            # T > 0 needs uniforms
+    assert call(logits=None) == d2sd.ERR_INVALID_ARG
+    assert call(logits=f + 8) == d2sd.ERR_INVALID_ARG                      # alignment
+    assert "aligned" in d2sd.last_error()
+    assert d2sd._sample(1, f, 10, 10, f, f, 100, d2sd.F32, f, 1.0, f, None, None, None) == d2sd.ERR_INVALID_ARG
+
+
 def good_args(**kw):
     a = d2sd.AttnArgs()
     a.batch, a.num_qo_heads, a.num_kv_heads, a.head_dim, a.page_size = 32, 32, 8, 128, 16

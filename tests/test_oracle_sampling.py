@@ -100,6 +100,8 @@ def test_edges():
     assert sample_token([-np.inf, 0.0, -np.inf, 0.0], 1.0, 0.0) == 1
     assert sample_token([-np.inf, 0.0, -np.inf, 0.0], 1.0, np.nextafter(1.0, 0.0)) == 3
     assert sample_token([0.0, 0.0, 0.0, -np.inf], 1.0, np.nextafter(1.0, 0.0)) == 2
+    for T in (0.0, 1.0):
+        assert sample_token([-np.inf] * 5, T, 0.5) == -1                # no distribution
 
 
 def test_temperature_is_a_logit_scale():
