@@ -113,6 +113,7 @@ def oracle_tree_arrays(trees, W, kmax=None):
 def max_abs(a, b):
     a = np.asarray(a, np.float64)
     b = np.asarray(b, np.float64)
-    both_inf = np.isneginf(a) & np.isneginf(b)
-    d = np.abs(np.where(both_inf, 0.0, a - b))
+    both_inf = np.isneginf(a) & np.isneginf(b)       # equal -inf (an empty side) counts as exact
+    with np.errstate(invalid="ignore"):
+        d = np.abs(np.where(both_inf, 0.0, a - b))
     return float(np.nan_to_num(d, nan=np.inf).max(initial=0.0))
