@@ -865,24 +865,23 @@ void cascade_bf16_kernel(Params p) {
 }
 
 // Log-sum-exp reduction of the split partials of every output row (rows of
-// single-split requests were finalised by the attention kernel). 32 threads
-// per row, 4 dims each.
+// single-split requests were finalised by the attention kernel). A workgroup
+// takes kMergeRows consecutive rows of one request (32 threads per row, 4
+// dims each): the request comes from the grid, so a thread needs only the
+// request's node range and context length before it reads the partials.
+static_assert(kMergeRows * 32 == kThreads, "32 threads per merged row");
+
 template <typename T>
-__global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p) {
-  const int total_rows = p.total_nodes * p.hq;
-  const int row = blockIdx.x * (kThreads / 32) + (threadIdx.x >> 5);
-  if (row >= total_rows) return;
-  const int node = row / p.hq;
-  // request of this node: last b with node_indptr[b] <= node
-  int lo = 0, hi = p.batch - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (p.node_indptr[mid] <= node) lo = mid; else hi = mid - 1;
-  }
-  const int b = lo;
+__global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p, int chunks) {
+  const int b = blockIdx.x / chunks;
+  const int chunk = blockIdx.x % chunks;
+  const int node_base = clampi(p.node_indptr[b], 0, p.total_nodes);
+  const int Nb = clampi(p.node_indptr[b + 1] - node_base, 0, min(p.max_nodes, p.total_nodes - node_base));
   const int Cb = clampi(p.ctx_len[b], 0, p.max_ctx);
   const int n_ch_b = max(1, ceil_div(Cb, p.split));
-  if (n_ch_b == 1) return;
+  const int r = chunk * kMergeRows + (threadIdx.x >> 5);   // row within the request
+  if (n_ch_b == 1 || r >= Nb * p.hq) return;
+  const int row = node_base * p.hq + r;
   const size_t stride = (size_t)p.total_nodes * p.hq;
   float M = -INFINITY;
   for (int s = 0; s < n_ch_b; ++s) M = fmaxf(M, p.ws_m[s * stride + row]);
@@ -962,12 +961,12 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
   if (ev1) (void)hipEventRecord(ev1, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || plan.n_ch_max <= 1) return e;
-  const long long rows = (long long)a.total_nodes * a.num_qo_heads;
-  const int mgrid = (int)((rows + (kThreads / 32) - 1) / (kThreads / 32));
+  const long long chunks = merge_chunks_per_request(a.max_nodes, a.num_qo_heads);
+  const dim3 mgrid((unsigned)(a.batch * chunks));
   if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(split_merge_kernel<__bf16>, dim3(mgrid), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(split_merge_kernel<__bf16>, mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
   else
-    hipLaunchKernelGGL(split_merge_kernel<float>, dim3(mgrid), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(split_merge_kernel<float>, mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
   return hipGetLastError();
 }
 

@@ -61,4 +61,11 @@ __host__ __device__ constexpr int group_rows(int dtype) {
   return (dtype == D2SD_BF16 ? kBf16Waves : 4) * kRowsPerTile;
 }
 
+// Rows per workgroup of the split-merge kernel, and its workgroups per
+// request (the grid is batch x this many).
+constexpr int kMergeRows = 8;
+__host__ __device__ inline long long merge_chunks_per_request(int max_nodes, int hq) {
+  return ((long long)max_nodes * hq + kMergeRows - 1) / kMergeRows;
+}
+
 }  // namespace d2sd
