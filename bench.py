@@ -57,6 +57,10 @@ def parse():
                          "(measured no faster than eager launches: the step is not launch-bound)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy three times (HBM counter calibration)")
+    ap.add_argument("--record-traffic", metavar="DIR",
+                    help="host only: derive the attention kernel's HBM bytes per launch from rocprofv3 counter "
+                         "CSVs under DIR (fetch/, write/, copy_fetch/, copy_write/, and fetch.log holding the "
+                         "profiled bench line) and write them to the traffic record read by later runs")
     return ap.parse_args()
 
 
@@ -102,6 +106,63 @@ def measured_traffic(config: int, kv_split: int, resolved_split: int):
             or r.get("resolved_kv_split") != resolved_split:
         return None
     return r.get("hbm_bytes_per_launch")
+
+
+def _counter_per_dispatch(csv_dir: str, kernel: str, counter: str) -> float:
+    """Mean over dispatches of `kernel` of the counter's value (summed over the
+    rows of each dispatch) in a rocprofv3 counter-collection CSV."""
+    import csv
+    import glob
+
+    paths = glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not paths:
+        raise FileNotFoundError(f"no counter_collection.csv under {csv_dir}")
+    per = {}
+    for path in paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if kernel in r["Kernel_Name"] and r["Counter_Name"] == counter:
+                    per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    if not per:
+        raise ValueError(f"no {counter} rows for {kernel} under {csv_dir}")
+    return sum(per.values()) / len(per)
+
+
+def record_traffic(d: str):
+    """Write the attention kernel's measured HBM bytes per launch. FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) are scaled by what they read for a 1 GiB
+    device copy (--copy-probe), so the factors come from the same counters."""
+    with open(os.path.join(d, "fetch.log")) as f:
+        line = [ln for ln in f.read().splitlines() if ln.startswith("{")][-1]
+    bench = json.loads(line)
+    kern = "cascade_bf16_kernel" if bench["dtype"] == "bf16" else "cascade_attention_kernel"
+    fetch = _counter_per_dispatch(os.path.join(d, "fetch"), kern, "FETCH_SIZE")
+    write = _counter_per_dispatch(os.path.join(d, "write"), kern, "WRITE_SIZE")
+    copy_kib = (1 << 30) / 1024.0
+    f_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_fetch"), "copyBuffer", "FETCH_SIZE")
+    w_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_write"), "copyBuffer", "WRITE_SIZE")
+    cfg = bench["config"]
+    cfg_num = next(k for k, v in _workload_names().items() if v == cfg["workload"])
+    rec = {}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    rec[f"config{cfg_num}"] = {
+        "workload": cfg["workload"], "kernel_sha": kernel_sha(), "kv_split": bench.get("requested_kv_split", 0),
+        "resolved_kv_split": cfg["kv_split"], "fetch_kib_per_dispatch": round(fetch, 1),
+        "write_kib_per_dispatch": round(write, 1), "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4),
+        "hbm_bytes_per_launch": int(round((fetch * f_fac + write * w_fac) * 1024)),
+        "summary": f"profiles/cascade_attention_{cfg['workload']}.md",
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec[f"config{cfg_num}"]), flush=True)
+
+
+def _workload_names() -> dict:
+    from paper_2606_04446_amd import workload as wl
+    return {k: v.name for k, v in wl.CONFIGS.items()}
 
 
 def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float, parents=None):
@@ -153,6 +214,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe()
+        return
+    if args.record_traffic:
+        record_traffic(args.record_traffic)
         return
 
     import torch
@@ -302,6 +366,7 @@ def main():
         "attn_kernel_ms": round(kern_ms, 4),
         "attn_tokens_per_s": round(total / t_s, 1),
         "kernel_sha": kernel_sha(),
+        "requested_kv_split": args.kv_split,
     }
     if args.noncascade:
         out2 = torch.empty_like(out)
