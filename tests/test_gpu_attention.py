@@ -63,6 +63,17 @@ def test_edge_shapes(dtype):
         check_full(case, stage)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_contexts_longer_than_one_split(dtype):
+    """Contexts past the longest split (32768 tokens) take several splits and
+    page ids past the first 2048 of a request; lengths are not multiples of
+    the page or tile size. Automatic split and the longest explicit one."""
+    lay = wl.custom_layout(16, [[3, 11], [1, 2, 14]], [70001, 33003], hq=8, hkv=2, dtype=dtype, seed=21)
+    case = Case(lay, poison_slack=True)
+    check_full(case)
+    check_full(case, "cascade", kv_split=32768)
+
+
 @pytest.mark.parametrize("hq,hkv", [(8, 8), (12, 4), (64, 8), (6, 1)])
 def test_gqa_groupings(hq, hkv):
     lay = wl.custom_layout(16, [[2, 9], [5, 6, 7, 8]], [200, 77], hq=hq, hkv=hkv, dtype="bf16", seed=13)
