@@ -9,6 +9,11 @@
 // length and the chosen node come from one max-reduction over the key
 // (depth, -index), which implements "deepest accepted node, lowest canonical
 // index on ties".
+//
+// The kernel is latency-bound (a few hundred nodes per request): every global
+// input of a node is read in one batch of independent loads at the start and
+// staged in LDS, so the match flags, the scan and the walk up the chosen path
+// never wait on global memory again.
 #include "launchers.h"
 
 namespace d2sd {
@@ -26,6 +31,12 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_path_kernel(
   __shared__ uint8_t s_ok[2][kMaxNodes];
   __shared__ short s_up[2][kMaxNodes];
   __shared__ short s_par[kMaxNodes];
+  __shared__ uint8_t s_dep[kMaxNodes];
+  __shared__ int s_tok[kMaxNodes];
+  __shared__ int s_arg[kMaxNodes];
+  __shared__ int s_pid[kMaxNodes];
+  __shared__ int s_pn[D2SD_MAX_B];
+  __shared__ int s_tk[D2SD_MAX_B];
   __shared__ int s_best[kAcceptThreads / kWave];
 
   const int b = blockIdx.x;
@@ -36,10 +47,21 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_path_kernel(
   for (int c = t; c < Nb; c += kAcceptThreads) {
     int par = parent[base + c];
     if (par < 0 || par >= c) par = -1;   // canonical order puts parents first
-    const bool ok = par < 0 || draft[base + c] == argmax[base + par];
-    s_ok[0][c] = ok;
-    s_up[0][c] = (short)par;
     s_par[c] = (short)par;
+    s_tok[c] = draft[base + c];
+    s_arg[c] = argmax[base + c];
+    s_pid[c] = path_id[base + c];
+    s_dep[c] = (uint8_t)clampi(depth[base + c], 0, B - 1);
+  }
+  if (t < B) {
+    s_pn[t] = -1;
+    s_tk[t] = -1;
+  }
+  __syncthreads();
+  for (int c = t; c < Nb; c += kAcceptThreads) {
+    const short par = s_par[c];
+    s_ok[0][c] = par < 0 || s_tok[c] == s_arg[par];
+    s_up[0][c] = par;
   }
   __syncthreads();
   int cur = 0;
@@ -61,38 +83,36 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_path_kernel(
   // key = depth * 65536 + (65535 - index) over accepted nodes; the root is
   // always accepted, so the maximum exists whenever Nb > 0.
   int best = -1;
-  for (int c = t; c < Nb; c += kAcceptThreads) {
-    if (s_ok[cur][c]) {
-      const int d = clampi(depth[base + c], 0, B - 1);
-      best = max(best, d * 65536 + (65535 - c));
-    }
-  }
+  for (int c = t; c < Nb; c += kAcceptThreads)
+    if (s_ok[cur][c]) best = max(best, (int)s_dep[c] * 65536 + (65535 - c));
   for (int off = kWave / 2; off > 0; off /= 2) best = max(best, __shfl_xor(best, off));
   if ((t % kWave) == 0) s_best[t / kWave] = best;
   __syncthreads();
 
   if (t == 0) {
     for (int w = 1; w < kAcceptThreads / kWave; ++w) best = max(best, s_best[w]);
-    int* pn = path_nodes + (size_t)b * B;
-    int* tk = out_tokens + (size_t)b * B;
-    for (int d = 0; d < B; ++d) { pn[d] = -1; tk[d] = -1; }
     if (best < 0) {
       accept_len[b] = 0; best_path[b] = 0; accept_node[b] = -1;
-      return;
+    } else {
+      const int L = best / 65536;
+      const int chosen = 65535 - best % 65536;
+      accept_len[b] = L;
+      best_path[b] = s_pid[chosen];
+      accept_node[b] = chosen;
+      // Walk up from the chosen node; depth L sits at slot L.
+      int c = chosen;
+      for (int d = L; d >= 0 && c >= 0; --d) {
+        s_pn[d] = c;
+        if (d >= 1) s_tk[d - 1] = s_tok[c];
+        c = s_par[c];
+      }
+      s_tk[L] = s_arg[chosen];
     }
-    const int L = best / 65536;
-    const int chosen = 65535 - best % 65536;
-    accept_len[b] = L;
-    best_path[b] = path_id[base + chosen];
-    accept_node[b] = chosen;
-    // Walk up from the chosen node; depth L sits at slot L.
-    int c = chosen;
-    for (int d = L; d >= 0 && c >= 0; --d) {
-      pn[d] = c;
-      if (d >= 1) tk[d - 1] = draft[base + c];
-      c = s_par[c];
-    }
-    tk[L] = argmax[base + chosen];
+  }
+  __syncthreads();
+  if (t < B) {
+    path_nodes[(size_t)b * B + t] = s_pn[t];
+    out_tokens[(size_t)b * B + t] = s_tk[t];
   }
 }
 

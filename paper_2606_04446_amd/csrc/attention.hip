@@ -6,28 +6,28 @@
 // Work decomposition. For one request b and KV head h, the M = N_b * G query
 // rows (tree node n, query head h*G+g, row index n*G+g) all attend to the same
 // context keys, so they are stacked into the column dimension of one dense
-// contraction. A workgroup (4 waves, one per SIMD) owns up to 8 column tiles
-// of 32 rows and one split of the context; every 64-key K/V tile of that
-// split is fetched from HBM once (128-bit coalesced loads of whole 4 KB page
-// slabs), staged in LDS and consumed by all its rows. The tree keys of the
-// request are appended to split 0 under the ancestor mask, so the tree state
-// joins the context state through the same online log-sum-exp rescale.
+// contraction. A work item is (request, KV head, row group, context split); a
+// row group is 128 rows, four waves of one 32-row column tile each. Every
+// 32-key K/V tile of the split is fetched from HBM once per row group, staged
+// in an LDS ring of two stages and consumed by all rows of the group. The tree
+// keys of the request are appended to split 0 under the ancestor mask, so the
+// tree state joins the context state through the same online log-sum-exp
+// rescale.
 //
 // Per tile and wave: S^T = K Q^T with MFMA (keys on the MFMA row axis,
 // queries on the column axis), so a lane owns one query and 16 keys of each
 // 32-key block; the row max needs one cross-half exchange and the row sum
 // stays lane-local. P^T leaves the accumulator already in MFMA B-operand
-// order; V is written to LDS transposed with the matching key permutation, so
-// O^T += V^T P^T needs no register shuffles. Split partials (unnormalised O,
-// running max in log2 units, running sum) go to the workspace and a second
-// kernel merges them by log-sum-exp; a request with a single split is
-// finalised in place.
+// order, and O^T += V^T P^T takes the V^T fragments in the matching key order
+// (bf16: transposing LDS reads of the row-major V tile; fp32: per-element
+// reads of the key-major tile). Split partials (unnormalised O, running max in
+// log2 units, running sum) go to the workspace and a second kernel merges them
+// by log-sum-exp; a request with a single split is finalised in place.
 //
-// bf16 kernel: 8 waves (two per SIMD), each owning one 32-query column tile of
-// the workgroup's 256 rows; the two waves sharing a SIMD overlap one's
-// exponentials with the other's matrix work. The running max is only moved
-// (and O, l rescaled) when it grows by more than 2^8, which keeps the rescale
-// off the common path; interior context tiles skip masking entirely.
+// The fp32 kernel stages tiles through registers. The bf16 kernel copies them
+// by LDS DMA, runs three 40 KB workgroups per CU (three independent waves per
+// SIMD), moves the running max (and rescales O and l) only when it grows by
+// more than 2^8, and skips masking on interior context tiles.
 #include <math.h>
 
 #include "common.h"

@@ -56,7 +56,6 @@ constexpr int kBf16Waves = 4;
 // the cascade kernel (one tile per wave: kBf16Waves for bf16, 4 for fp32);
 // the host planner and the kernels must agree on them.
 constexpr int kRowsPerTile = 32;
-constexpr int kTilesPerGroup = 8;
 __host__ __device__ constexpr int group_rows(int dtype) {
   return (dtype == D2SD_BF16 ? kBf16Waves : 4) * kRowsPerTile;
 }

@@ -20,18 +20,24 @@ __global__ __launch_bounds__(kTreeThreads) void tree_build_kernel(
     const int* __restrict__ node_indptr, int total_nodes, int mask_words, int* __restrict__ parent,
     int* __restrict__ depth, int* __restrict__ path_id, uint32_t* __restrict__ anc_mask,
     int* __restrict__ path_leaf) {
+  __shared__ int s_raw[D2SD_MAX_B];    // positions as given
   __shared__ int s_p[D2SD_MAX_B];      // positions sorted ascending
   __shared__ int s_off[D2SD_MAX_B + 1];
   const int b = blockIdx.x;
   const int t = threadIdx.x;
+  // All global inputs in one batch of independent loads: the row of p is
+  // read whole (it is Kmax entries long whatever K[b] is), then ranked in LDS.
   const int Kb = clampi(K[b], 0, min(Kmax, B - 1));
+  const int ip0 = node_indptr[b], ip1 = node_indptr[b + 1];
+  if (t < min(Kmax, B - 1)) s_raw[t] = clampi(p[(size_t)b * Kmax + t], 1, B - 1);
+  __syncthreads();
 
   // Rank sort: positions are distinct, so rank = number of smaller positions.
   if (t < Kb) {
-    const int pt = clampi(p[(size_t)b * Kmax + t], 1, B - 1);
+    const int pt = s_raw[t];
     int rank = 0;
     for (int j = 0; j < Kb; ++j) {
-      const int pj = clampi(p[(size_t)b * Kmax + j], 1, B - 1);
+      const int pj = s_raw[j];
       rank += (pj < pt) || (pj == pt && j < t);
     }
     s_p[rank] = pt;
@@ -47,8 +53,8 @@ __global__ __launch_bounds__(kTreeThreads) void tree_build_kernel(
   }
   __syncthreads();
 
-  const int base = clampi(node_indptr[b], 0, total_nodes);
-  const int Nb = clampi(min(s_off[Kb], node_indptr[b + 1] - base), 0, total_nodes - base);
+  const int base = clampi(ip0, 0, total_nodes);
+  const int Nb = clampi(min(s_off[Kb], ip1 - base), 0, total_nodes - base);
   for (int n = t; n < Nb; n += kTreeThreads) {
     int pos, path, par, main_hi, br_lo, br_hi;
     if (n < B) {
