@@ -866,10 +866,13 @@ void cascade_bf16_kernel(Params p) {
 
 // Log-sum-exp reduction of the split partials of every output row (rows of
 // single-split requests were finalised by the attention kernel). A workgroup
-// takes kMergeRows consecutive rows of one request (32 threads per row, 4
+// takes kMergeRows consecutive rows of one request (16 threads per row, 8
 // dims each): the request comes from the grid, so a thread needs only the
-// request's node range and context length before it reads the partials.
-static_assert(kMergeRows * 32 == kThreads, "32 threads per merged row");
+// request's node range and context length before it reads the partials. The
+// splits are folded in one pass with a running max, so the loads of one
+// split do not wait on the values of the previous one and the unrolled loop
+// keeps several splits' partials in flight.
+static_assert(kMergeRows * 16 == kThreads, "16 threads per merged row");
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p, int chunks) {
@@ -879,27 +882,38 @@ __global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p, int chu
   const int Nb = clampi(p.node_indptr[b + 1] - node_base, 0, min(p.max_nodes, p.total_nodes - node_base));
   const int Cb = clampi(p.ctx_len[b], 0, p.max_ctx);
   const int n_ch_b = max(1, ceil_div(Cb, p.split));
-  const int r = chunk * kMergeRows + (threadIdx.x >> 5);   // row within the request
+  const int r = chunk * kMergeRows + (threadIdx.x >> 4);   // row within the request
   if (n_ch_b == 1 || r >= Nb * p.hq) return;
   const int row = node_base * p.hq + r;
   const size_t stride = (size_t)p.total_nodes * p.hq;
-  float M = -INFINITY;
-  for (int s = 0; s < n_ch_b; ++s) M = fmaxf(M, p.ws_m[s * stride + row]);
-  const float Mu = M == -INFINITY ? 0.0f : M;
-  const int d0 = (threadIdx.x & 31) * 4;
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  float L = 0.0f;
+  const int d0 = (threadIdx.x & 15) * 8;
+  float M = -INFINITY, L = 0.0f;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
   for (int s = 0; s < n_ch_b; ++s) {
     const size_t pr = s * stride + row;
-    const float w = __builtin_amdgcn_exp2f(p.ws_m[pr] - Mu);
-    L += w * p.ws_l[pr];
-    const float4 v = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0);
-    acc[0] += w * v.x; acc[1] += w * v.y; acc[2] += w * v.z; acc[3] += w * v.w;
+    const float ms = p.ws_m[pr];
+    const float ls = p.ws_l[pr];
+    const float4 v0 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0);
+    const float4 v1 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0 + 4);
+    const float Mn = fmaxf(M, ms);
+    if (Mn == -INFINITY) continue;                        // no keys so far
+    const float a = __builtin_amdgcn_exp2f(M - Mn);       // 0 while M is -inf
+    const float w = __builtin_amdgcn_exp2f(ms - Mn);      // 0 for an empty split
+    const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    L = L * a + w * ls;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = acc[i] * a + w * v[i];
+    M = Mn;
   }
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  float v[4] = {acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
-  store_out<T>(static_cast<T*>(p.out) + (size_t)row * kD + d0, v);
-  if (p.lse && (threadIdx.x & 31) == 0) p.lse[row] = L > 0.0f ? (M + __log2f(L)) * kLn2 : -INFINITY;
+  float o[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = acc[i] * inv;
+  T* dst = static_cast<T*>(p.out) + (size_t)row * kD + d0;
+  store_out<T>(dst, o);
+  store_out<T>(dst + 4, o + 4);
+  if (p.lse && (threadIdx.x & 15) == 0) p.lse[row] = L > 0.0f ? (M + __log2f(L)) * kLn2 : -INFINITY;
 }
 
 // The cascade merge as a standalone operator: merge two normalised states.

@@ -62,7 +62,7 @@ __host__ __device__ constexpr int group_rows(int dtype) {
 
 // Rows per workgroup of the split-merge kernel, and its workgroups per
 // request (the grid is batch x this many).
-constexpr int kMergeRows = 8;
+constexpr int kMergeRows = 16;
 __host__ __device__ inline long long merge_chunks_per_request(int max_nodes, int hq) {
   return ((long long)max_nodes * hq + kMergeRows - 1) / kMergeRows;
 }
