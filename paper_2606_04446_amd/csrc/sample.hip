@@ -11,11 +11,16 @@
 // the request's parent and token arrays (staged in LDS), then streams the
 // representative's logits row once: every wave reduces 2048 (bf16) or 1024
 // (fp32) consecutive logits per step to a (max, sum of exp) pair, or to
-// (max, first index of the max) for T = 0, kept in LDS per step. Wave 0 then
-// scans the step sums in vocabulary order, finds the step where the running
-// sum crosses u times the total, and re-reads only that step to find the
-// token inside it. The row is read from HBM once; the cost is one pass of
-// loads plus one exponential per logit.
+// (max, first index of the max) for T = 0, kept in LDS per step. The loads of
+// two of a wave's steps are issued together, before either is reduced, and
+// the first of them go out before the representative search: a node is
+// nearly always its own representative, and otherwise they are issued again
+// for the representative's row. Wave 0 then scans the step sums in
+// vocabulary order, finds the step where the running sum crosses u times the
+// total, and re-reads only that step to find the token inside it. Wave
+// reductions and scans run on DPP and the lane-pair swaps, not through LDS.
+// The row is read from HBM once; the cost is one pass of loads plus one
+// exponential per logit.
 #include "launchers.h"
 
 namespace d2sd {
@@ -25,6 +30,7 @@ namespace {
 constexpr int kSampleThreads = 256;
 constexpr int kSampleWaves = kSampleThreads / kWave;
 constexpr int kLoadsPerStep = 4;                                   // 16-byte loads per lane per step
+constexpr int kResident = 2;                                       // steps per wave whose loads are in flight together
 constexpr int kMaxSteps = D2SD_MAX_VOCAB / (kWave * kLoadsPerStep * 4);   // fp32 steps hold the fewest logits
 constexpr int kMaxNodes = D2SD_MAX_B + D2SD_MAX_B * (D2SD_MAX_B - 1) / 2;   // 2080
 constexpr int kNoIndex = 0x7fffffff;
@@ -32,24 +38,36 @@ constexpr int kNoIndex = 0x7fffffff;
 template <int DT>
 struct Logits;
 
+// The logits of elements start .. start + kVec - 1, still packed; elements at
+// or past V read as -inf. load_elems loads element by element at indices
+// clamped into the row, with no branch, so all loads of a step are issued
+// before any is used; load_raw takes one 16-byte load when the row is aligned
+// and the chunk lies inside it.
 template <>
 struct Logits<D2SD_BF16> {
   static constexpr int kVec = 8;
-  // Eight logits from element `start` on; elements at or past V read as -inf.
-  __device__ static __forceinline__ void load(const void* row, long long start, int V, bool vec_ok, float* v) {
+  __device__ static __forceinline__ uint4 load_raw(const void* row, long long start, int V, bool vec_ok) {
     const uint16_t* r = static_cast<const uint16_t*>(row);
-    if (vec_ok && start + kVec <= V) {
-      const uint4 x = *reinterpret_cast<const uint4*>(r + start);
-      const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+    if (vec_ok && start + kVec <= V) return *reinterpret_cast<const uint4*>(r + start);
+    return load_elems(row, start, V);
+  }
+  __device__ static __forceinline__ uint4 load_elems(const void* row, long long start, int V) {
+    const uint16_t* r = static_cast<const uint16_t*>(row);
+    uint32_t e[kVec];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        v[2 * i] = __uint_as_float(w[i] << 16);
-        v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-      }
-    } else {
+    for (int i = 0; i < kVec; ++i) e[i] = r[min(start + i, (long long)V - 1)];
+    uint32_t w[4];
 #pragma unroll
-      for (int e = 0; e < kVec; ++e)
-        v[e] = start + e < V ? __uint_as_float((uint32_t)r[start + e] << 16) : -INFINITY;
+    for (int i = 0; i < 4; ++i)
+      w[i] = (start + 2 * i < V ? e[2 * i] : 0xff80u) | ((start + 2 * i + 1 < V ? e[2 * i + 1] : 0xff80u) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  __device__ static __forceinline__ void unpack(const uint4& x, float* v) {
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
     }
   }
 };
@@ -57,45 +75,96 @@ struct Logits<D2SD_BF16> {
 template <>
 struct Logits<D2SD_F32> {
   static constexpr int kVec = 4;
-  __device__ static __forceinline__ void load(const void* row, long long start, int V, bool vec_ok, float* v) {
+  __device__ static __forceinline__ uint4 load_raw(const void* row, long long start, int V, bool vec_ok) {
     const float* r = static_cast<const float*>(row);
-    if (vec_ok && start + kVec <= V) {
-      const float4 x = *reinterpret_cast<const float4*>(r + start);
-      v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-    } else {
+    if (vec_ok && start + kVec <= V) return *reinterpret_cast<const uint4*>(r + start);
+    return load_elems(row, start, V);
+  }
+  __device__ static __forceinline__ uint4 load_elems(const void* row, long long start, int V) {
+    const float* r = static_cast<const float*>(row);
+    float e[kVec];
 #pragma unroll
-      for (int e = 0; e < kVec; ++e) v[e] = start + e < V ? r[start + e] : -INFINITY;
-    }
+    for (int i = 0; i < kVec; ++i) e[i] = r[min(start + i, (long long)V - 1)];
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < kVec; ++i) w[i] = __float_as_uint(start + i < V ? e[i] : -INFINITY);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  __device__ static __forceinline__ void unpack(const uint4& x, float* v) {
+    v[0] = __uint_as_float(x.x); v[1] = __uint_as_float(x.y);
+    v[2] = __uint_as_float(x.z); v[3] = __uint_as_float(x.w);
   }
 };
 
+template <int DT>
+__device__ __forceinline__ void load_logits(const void* row, long long start, int V, bool vec_ok, float* v) {
+  Logits<DT>::unpack(Logits<DT>::load_raw(row, start, V, vec_ok), v);
+}
+
+// Cross-lane reductions and scans on DPP (inside rows of 16 lanes) and the
+// lane-pair swaps (across rows): register to register, with no LDS round trip
+// per level. Every lane of a reduction combines the same operands in the same
+// order, so all lanes end with identical bits.
+constexpr int kQuadSwap1 = 0xB1;      // DPP quad_perm [1,0,3,2]
+constexpr int kQuadSwap2 = 0x4E;      // DPP quad_perm [2,3,0,1]
+constexpr int kRowMirror = 0x140;     // lane i <- lane 15 - i of its row
+constexpr int kRowHalfMirror = 0x141; // lane i <- lane 7 - i of its half row
+constexpr int kRowShr = 0x110;        // + n: lane i <- lane i - n of its row
+constexpr int kRowBcast15 = 0x142;    // lane 15 of a row -> every lane of the next row
+constexpr int kRowBcast31 = 0x143;    // lane 31 -> every lane of rows 2 and 3
+
+// Lanes without a source lane, or outside the row mask, return `old`.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp(uint32_t old, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROW_MASK, 0xf, false);
+}
+
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, Op op) {
+  x = op(x, dpp<kQuadSwap1>(x, x));
+  x = op(x, dpp<kQuadSwap2>(x, x));
+  x = op(x, dpp<kRowHalfMirror>(x, x));
+  x = op(x, dpp<kRowMirror>(x, x));
+  const auto r16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);   // {lane with bit 4 clear, set}
+  x = op(r16[0], r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);   // {lane with bit 5 clear, set}
+  return op(r32[0], r32[1]);
+}
+
 __device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off /= 2) x = fmaxf(x, __shfl_xor(x, off));
-  return x;
+  return __uint_as_float(wave_reduce(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
 }
 
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off /= 2) x += __shfl_xor(x, off);
-  return x;
+  return __uint_as_float(wave_reduce(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
 }
 
 __device__ __forceinline__ int wave_min(int x) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off /= 2) x = min(x, __shfl_xor(x, off));
+  return (int)wave_reduce((uint32_t)x, [](uint32_t a, uint32_t b) { return (uint32_t)min((int)a, (int)b); });
+}
+
+// Inclusive prefix sum over the lanes of a wave, in lane order: a
+// Hillis-Steele scan inside each row of 16, then the totals of rows 0 and 2
+// into rows 1 and 3, then the total of rows 0-1 into rows 2 and 3.
+__device__ __forceinline__ float wave_inclusive_scan(float x) {
+  x += __uint_as_float(dpp<kRowShr + 1>(0u, __float_as_uint(x)));
+  x += __uint_as_float(dpp<kRowShr + 2>(0u, __float_as_uint(x)));
+  x += __uint_as_float(dpp<kRowShr + 4>(0u, __float_as_uint(x)));
+  x += __uint_as_float(dpp<kRowShr + 8>(0u, __float_as_uint(x)));
+  x += __uint_as_float(dpp<kRowBcast15, 0xa>(0u, __float_as_uint(x)));
+  x += __uint_as_float(dpp<kRowBcast31, 0xc>(0u, __float_as_uint(x)));
   return x;
 }
 
-// Inclusive prefix sum over the lanes of a wave, in lane order.
-__device__ __forceinline__ float wave_inclusive_scan(float x, int lane) {
-#pragma unroll
-  for (int off = 1; off < kWave; off *= 2) {
-    const float y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  return x;
+// Value of x in lane `src` (uniform over the wave).
+__device__ __forceinline__ float lane_value(float x, int src) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), src));
 }
+__device__ __forceinline__ int lane_value(int x, int src) { return __builtin_amdgcn_readlane(x, src); }
 
 __device__ __forceinline__ int first_lane(uint64_t mask) { return mask ? __ffsll((long long)mask) - 1 : -1; }
 
@@ -116,6 +185,59 @@ __device__ __forceinline__ float step_scale(float ms, float mx, float k2) {
 template <int VEC>
 __device__ __forceinline__ int step_index(int s, int lane, int i) {
   return s * (kWave * kLoadsPerStep * VEC) + (i / VEC) * (kWave * VEC) + lane * VEC + (i % VEC);
+}
+
+// Issue the loads of kResident whole steps of a wave (steps s0, s0 + waves,
+// ...) of an aligned row: plain 16-byte loads under a wave-uniform bound.
+template <int DT>
+__device__ __forceinline__ void load_full(uint4 (&raw)[kResident][kLoadsPerStep], const void* rowp, int s0,
+                                          int n_full, int lane) {
+  constexpr int VEC = Logits<DT>::kVec;
+  const uint4* r = static_cast<const uint4*>(rowp);
+#pragma unroll
+  for (int j = 0; j < kResident; ++j) {
+    const int s = s0 + j * kSampleWaves;
+    if (s < n_full) {
+#pragma unroll
+      for (int k = 0; k < kLoadsPerStep; ++k) raw[j][k] = r[step_index<VEC>(s, lane, k * VEC) / VEC];
+    }
+  }
+}
+
+// One step's (max, sum of exp relative to it) or, for T = 0, (max, first
+// index of the max), kept in LDS by lane 0.
+template <int DT>
+__device__ __forceinline__ void reduce_step(const uint4 (&raw)[kLoadsPerStep], int s, int lane, int greedy,
+                                            float k2, float* s_m, float* s_x) {
+  constexpr int VEC = Logits<DT>::kVec;
+  constexpr int NE = kLoadsPerStep * VEC;
+  float v[NE];
+#pragma unroll
+  for (int k = 0; k < kLoadsPerStep; ++k) Logits<DT>::unpack(raw[k], v + k * VEC);
+  float lm = v[0];
+#pragma unroll
+  for (int i = 1; i < NE; ++i) lm = fmaxf(lm, v[i]);
+  const float m = wave_max(lm);
+  float x;
+  if (greedy) {
+    int first = kNoIndex;                    // elements of a lane ascend with i
+#pragma unroll
+    for (int i = NE - 1; i >= 0; --i)
+      if (v[i] == m) first = step_index<VEC>(s, lane, i);
+    x = __int_as_float(m == -INFINITY ? kNoIndex : wave_min(first));
+  } else {
+    float sum = 0.0f;
+    if (m != -INFINITY) {
+      const float moff = step_offset(m, k2);
+#pragma unroll
+      for (int i = 0; i < NE; ++i) sum += __builtin_amdgcn_exp2f(fmaf(v[i], k2, -moff));
+    }
+    x = wave_sum(sum);
+  }
+  if (lane == 0) {
+    s_m[s] = m;
+    s_x[s] = x;
+  }
 }
 
 template <int DT>
@@ -149,6 +271,15 @@ __global__ __launch_bounds__(kSampleThreads) void sample_targets_kernel(
     s_par[x] = (short)par;
     s_tok[x] = draft[base + x];
   }
+  // The node is usually its own representative: the first loads of its row go
+  // out now (after the staging above, whose wait would otherwise include
+  // them) and are in flight during the search below.
+  const int n_steps = ceil_div(V, SE);
+  const int n_whole = V / SE;                   // steps lying wholly inside the row
+  const void* row_c = static_cast<const char*>(logits) + (size_t)(base + c) * (size_t)V * kEltBytes;
+  const bool vec_ok_c = ((size_t)(base + c) * (size_t)V) % VEC == 0;   // the row starts 16-byte aligned
+  uint4 raw[kResident][kLoadsPerStep];
+  load_full<DT>(raw, row_c, w, vec_ok_c ? n_whole : 0, lane);
   __syncthreads();
   if (t == 0) {
     int x = c, d = 0;
@@ -184,37 +315,27 @@ __global__ __launch_bounds__(kSampleThreads) void sample_targets_kernel(
   // ---- one pass over the representative's row: per-step (max, sum) or (max, index)
   const size_t row = (size_t)(base + rep);
   const void* rowp = static_cast<const char*>(logits) + row * (size_t)V * kEltBytes;
-  const bool vec_ok = (row * (size_t)V) % VEC == 0;   // the row starts 16-byte aligned
-  const int n_steps = ceil_div(V, SE);
+  const bool vec_ok = (row * (size_t)V) % VEC == 0;
+  // A wave takes steps w, w + 4, ...: the whole steps of an aligned row in
+  // batches of kResident whose loads are issued together, then the rest (a
+  // ragged last step, or every step of an unaligned row) element by element.
+  const int n_full = vec_ok ? n_whole : 0;
+  if (rep != c) load_full<DT>(raw, rowp, w, n_full, lane);
+  for (int s0 = w; s0 < n_full; s0 += kSampleWaves * kResident) {
+    if (s0 != w) load_full<DT>(raw, rowp, s0, n_full, lane);
+#pragma unroll
+    for (int j = 0; j < kResident; ++j) {
+      const int s = s0 + j * kSampleWaves;
+      if (s < n_full) reduce_step<DT>(raw[j], s, lane, greedy, k2, s_m, s_x);
+    }
+  }
   for (int s = w; s < n_steps; s += kSampleWaves) {
-    float v[NE];
+    if (s < n_full) continue;
+    uint4 tail[kLoadsPerStep];
 #pragma unroll
     for (int k = 0; k < kLoadsPerStep; ++k)
-      Logits<DT>::load(rowp, (long long)step_index<VEC>(s, lane, k * VEC), V, vec_ok, v + k * VEC);
-    float lm = v[0];
-#pragma unroll
-    for (int i = 1; i < NE; ++i) lm = fmaxf(lm, v[i]);
-    const float m = wave_max(lm);
-    float x;
-    if (greedy) {
-      int first = kNoIndex;                    // elements of a lane ascend with i
-#pragma unroll
-      for (int i = NE - 1; i >= 0; --i)
-        if (v[i] == m) first = step_index<VEC>(s, lane, i);
-      x = __int_as_float(m == -INFINITY ? kNoIndex : wave_min(first));
-    } else {
-      float sum = 0.0f;
-      if (m != -INFINITY) {
-        const float moff = step_offset(m, k2);
-#pragma unroll
-        for (int i = 0; i < NE; ++i) sum += __builtin_amdgcn_exp2f(fmaf(v[i], k2, -moff));
-      }
-      x = wave_sum(sum);
-    }
-    if (lane == 0) {
-      s_m[s] = m;
-      s_x[s] = x;
-    }
+      tail[k] = Logits<DT>::load_elems(rowp, (long long)step_index<VEC>(s, lane, k * VEC), V);
+    reduce_step<DT>(tail, s, lane, greedy, k2, s_m, s_x);
   }
   __syncthreads();
   if (w != 0) return;
@@ -238,20 +359,20 @@ __global__ __launch_bounds__(kSampleThreads) void sample_targets_kernel(
       return s < n_steps && s_x[s] > 0.0f ? s_x[s] * step_scale(s_m[s], mx, k2) : 0.0f;
     };
     float total = 0.0f;
-    for (int s0 = 0; s0 < n_steps; s0 += kWave) total += __shfl(wave_inclusive_scan(weight(s0 + lane), lane), kWave - 1);
+    for (int s0 = 0; s0 < n_steps; s0 += kWave) total += lane_value(wave_inclusive_scan(weight(s0 + lane)), kWave - 1);
     const float target = uniform[row] * total;
     int sel = -1;
     float before = 0.0f;                       // running sum before step sel
     float carry = 0.0f;
     for (int s0 = 0; s0 < n_steps && sel < 0; s0 += kWave) {
       const float a = weight(s0 + lane);
-      const float cum = carry + wave_inclusive_scan(a, lane);
+      const float cum = carry + wave_inclusive_scan(a);
       const int f = first_lane(__ballot(cum > target));
       if (f >= 0) {
         sel = s0 + f;
-        before = __shfl(cum - a, f);
+        before = lane_value(cum - a, f);
       }
-      carry = __shfl(cum, kWave - 1);
+      carry = lane_value(cum, kWave - 1);
     }
     int last_pos = -1;                         // rounding left no crossing: last step of positive weight
     if (sel < 0) {
@@ -266,7 +387,7 @@ __global__ __launch_bounds__(kSampleThreads) void sample_targets_kernel(
       float v[NE];
 #pragma unroll
       for (int k = 0; k < kLoadsPerStep; ++k)
-        Logits<DT>::load(rowp, (long long)step_index<VEC>(sel, lane, k * VEC), V, vec_ok, v + k * VEC);
+        load_logits<DT>(rowp, (long long)step_index<VEC>(sel, lane, k * VEC), V, vec_ok, v + k * VEC);
       const float ms = s_m[sel];
       const float moff = step_offset(ms, k2);
       const float scale = step_scale(ms, mx, k2);
@@ -284,15 +405,15 @@ __global__ __launch_bounds__(kSampleThreads) void sample_targets_kernel(
           incl[e] = acc;
           if (we > 0.0f) last = step_index<VEC>(sel, lane, k * VEC + e);
         }
-        const float lane_incl = wave_inclusive_scan(acc, lane);
+        const float lane_incl = wave_inclusive_scan(acc);
         const float lane_excl = run + lane_incl - acc;
         int hit = -1;
 #pragma unroll
         for (int e = VEC - 1; e >= 0; --e)
           if (lane_excl + incl[e] > rel) hit = e;
         const int f = first_lane(__ballot(hit >= 0));
-        if (f >= 0 && token < 0) token = step_index<VEC>(sel, f, k * VEC + __shfl(hit, f));
-        run += __shfl(lane_incl, kWave - 1);
+        if (f >= 0 && token < 0) token = step_index<VEC>(sel, f, k * VEC + lane_value(hit, f));
+        run += lane_value(lane_incl, kWave - 1);
       }
       if (token < 0) token = -wave_min(-last);  // last token of positive weight in the step
     }
