@@ -161,7 +161,10 @@ d2sd_status make_plan(const d2sd_attn_args* a, d2sd::AttnPlan* plan) {
   plan->n_rg_max = (int)max(1ll, (max_rows + rows_per_group - 1) / rows_per_group);
   plan->items = (long long)a->batch * a->num_kv_heads * plan->n_ch_max * plan->n_rg_max;
   if (plan->items > (1ll << 30)) return fail(D2SD_ERR_UNSUPPORTED, "too many work items (%lld)", plan->items);
-  if (plan->n_ch_max > 1 && (long long)a->batch * d2sd::merge_chunks_per_request(a->max_nodes, a->num_qo_heads) > (1ll << 30))
+  if (plan->n_ch_max > 1 &&
+      (long long)a->batch *
+              d2sd::merge_chunks_per_request(a->max_nodes, a->num_qo_heads, d2sd::merge_groups(plan->n_ch_max)) >
+          (1ll << 30))
     return fail(D2SD_ERR_UNSUPPORTED, "too many split-merge workgroups (batch %d, max_nodes %d)", a->batch,
                 a->max_nodes);
   const size_t rows = (size_t)a->total_nodes * a->num_qo_heads;

@@ -865,47 +865,83 @@ void cascade_bf16_kernel(Params p) {
 }
 
 // Log-sum-exp reduction of the split partials of every output row (rows of
-// single-split requests were finalised by the attention kernel). A workgroup
-// takes kMergeRows consecutive rows of one request (16 threads per row, 8
-// dims each): the request comes from the grid, so a thread needs only the
-// request's node range and context length before it reads the partials. The
-// splits are folded in one pass with a running max, so the loads of one
-// split do not wait on the values of the previous one and the unrolled loop
-// keeps several splits' partials in flight.
-static_assert(kMergeRows * 16 == kThreads, "16 threads per merged row");
+// single-split requests were finalised by the attention kernel). A row takes
+// GROUPS groups of 16 threads (8 dims per thread); group g folds splits g,
+// g + GROUPS, ... in one pass with a running max, so the loads of one split
+// never wait on the values of another and the unrolled loop keeps several
+// splits in flight; with several groups their states are then combined in
+// group order through LDS. A workgroup takes merge_rows(GROUPS) consecutive
+// rows of one request: the request comes from the grid, so a thread needs
+// only the request's node range and context length before it reads the
+// partials. Many splits (short contexts in small batches) take four groups,
+// which shortens the chain per thread and gives small batches more
+// workgroups.
+struct MergeState {
+  float m, l;
+  float acc[8];
+};
 
-template <typename T>
+template <typename T, int GROUPS>
 __global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p, int chunks) {
+  constexpr int ROWS = merge_rows(GROUPS);
+  static_assert(ROWS * GROUPS * 16 == kThreads, "16 threads per group and row");
+  __shared__ MergeState s_st[GROUPS > 1 ? kThreads : 1];
   const int b = blockIdx.x / chunks;
   const int chunk = blockIdx.x % chunks;
   const int node_base = clampi(p.node_indptr[b], 0, p.total_nodes);
   const int Nb = clampi(p.node_indptr[b + 1] - node_base, 0, min(p.max_nodes, p.total_nodes - node_base));
   const int Cb = clampi(p.ctx_len[b], 0, p.max_ctx);
   const int n_ch_b = max(1, ceil_div(Cb, p.split));
-  const int r = chunk * kMergeRows + (threadIdx.x >> 4);   // row within the request
-  if (n_ch_b == 1 || r >= Nb * p.hq) return;
+  const int rl = threadIdx.x / (16 * GROUPS);            // row within the workgroup
+  const int g = (threadIdx.x / 16) % GROUPS;             // split group
+  const int d0 = (threadIdx.x & 15) * 8;
+  const int r = chunk * ROWS + rl;                        // row within the request
+  const bool live = n_ch_b > 1 && r < Nb * p.hq;
   const int row = node_base * p.hq + r;
   const size_t stride = (size_t)p.total_nodes * p.hq;
-  const int d0 = (threadIdx.x & 15) * 8;
   float M = -INFINITY, L = 0.0f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (live) {
 #pragma unroll 4
-  for (int s = 0; s < n_ch_b; ++s) {
-    const size_t pr = s * stride + row;
-    const float ms = p.ws_m[pr];
-    const float ls = p.ws_l[pr];
-    const float4 v0 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0);
-    const float4 v1 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0 + 4);
-    const float Mn = fmaxf(M, ms);
-    if (Mn == -INFINITY) continue;                        // no keys so far
-    const float a = __builtin_amdgcn_exp2f(M - Mn);       // 0 while M is -inf
-    const float w = __builtin_amdgcn_exp2f(ms - Mn);      // 0 for an empty split
-    const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    L = L * a + w * ls;
+    for (int s = g; s < n_ch_b; s += GROUPS) {
+      const size_t pr = s * stride + row;
+      const float ms = p.ws_m[pr];
+      const float ls = p.ws_l[pr];
+      const float4 v0 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0);
+      const float4 v1 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0 + 4);
+      const float Mn = fmaxf(M, ms);
+      if (Mn == -INFINITY) continue;                        // no keys so far
+      const float a = __builtin_amdgcn_exp2f(M - Mn);       // 0 while M is -inf
+      const float w = __builtin_amdgcn_exp2f(ms - Mn);      // 0 for an empty split
+      const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      L = L * a + w * ls;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = acc[i] * a + w * v[i];
-    M = Mn;
+      for (int i = 0; i < 8; ++i) acc[i] = acc[i] * a + w * v[i];
+      M = Mn;
+    }
   }
+  if constexpr (GROUPS > 1) {
+    MergeState& st = s_st[threadIdx.x];
+    st.m = M;
+    st.l = L;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) st.acc[i] = acc[i];
+    __syncthreads();
+    if (g != 0) return;
+#pragma unroll
+    for (int gg = 1; gg < GROUPS; ++gg) {
+      const MergeState& o = s_st[threadIdx.x + 16 * gg];
+      const float Mn = fmaxf(M, o.m);
+      if (Mn == -INFINITY) continue;
+      const float a = __builtin_amdgcn_exp2f(M - Mn);
+      const float w = __builtin_amdgcn_exp2f(o.m - Mn);
+      L = L * a + w * o.l;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] = acc[i] * a + w * o.acc[i];
+      M = Mn;
+    }
+  }
+  if (!live) return;
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
   float o[8];
 #pragma unroll
@@ -975,12 +1011,20 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
   if (ev1) (void)hipEventRecord(ev1, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || plan.n_ch_max <= 1) return e;
-  const long long chunks = merge_chunks_per_request(a.max_nodes, a.num_qo_heads);
+  const int groups = merge_groups(plan.n_ch_max);
+  const long long chunks = merge_chunks_per_request(a.max_nodes, a.num_qo_heads, groups);
   const dim3 mgrid((unsigned)(a.batch * chunks));
-  if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(split_merge_kernel<__bf16>, mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
-  else
-    hipLaunchKernelGGL(split_merge_kernel<float>, mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+  if (a.dtype == D2SD_BF16) {
+    if (groups > 1)
+      hipLaunchKernelGGL((split_merge_kernel<__bf16, 4>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+    else
+      hipLaunchKernelGGL((split_merge_kernel<__bf16, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+  } else {
+    if (groups > 1)
+      hipLaunchKernelGGL((split_merge_kernel<float, 4>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+    else
+      hipLaunchKernelGGL((split_merge_kernel<float, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+  }
   return hipGetLastError();
 }
 

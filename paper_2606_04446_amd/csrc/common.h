@@ -60,11 +60,14 @@ __host__ __device__ constexpr int group_rows(int dtype) {
   return (dtype == D2SD_BF16 ? kBf16Waves : 4) * kRowsPerTile;
 }
 
-// Rows per workgroup of the split-merge kernel, and its workgroups per
-// request (the grid is batch x this many).
-constexpr int kMergeRows = 16;
-__host__ __device__ inline long long merge_chunks_per_request(int max_nodes, int hq) {
-  return ((long long)max_nodes * hq + kMergeRows - 1) / kMergeRows;
+// Split merge: 16 lanes per output row (8 dims each) and kMergeGroups(n)
+// groups of them per row, each folding every kMergeGroups-th split; a
+// workgroup of 256 threads then takes merge_rows(n) rows, and the grid is
+// batch x merge_chunks_per_request(...) workgroups.
+__host__ __device__ constexpr int merge_groups(int n_ch_max) { return n_ch_max >= 4 ? 4 : 1; }
+__host__ __device__ constexpr int merge_rows(int groups) { return 256 / (16 * groups); }
+__host__ __device__ inline long long merge_chunks_per_request(int max_nodes, int hq, int groups) {
+  return ((long long)max_nodes * hq + merge_rows(groups) - 1) / merge_rows(groups);
 }
 
 }  // namespace d2sd
