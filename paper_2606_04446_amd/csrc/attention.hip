@@ -448,7 +448,7 @@ constexpr int MAX_SPLIT_PAGES = 2048;    // page ids of one context split staged
 constexpr int KT = 32;                   // keys per tile (a 40 KB workgroup: three per CU)
 constexpr int NKB = KT / 32;             // 32-key MFMA blocks per tile
 constexpr int ROW_BYTES = kD * 2;        // 256 B per key row
-constexpr int TILE_BYTES = KT * ROW_BYTES;  // 16 KB for K (and for V)
+constexpr int TILE_BYTES = KT * ROW_BYTES;  // 8 KB for K (and for V)
 constexpr int BLOCKS = KT / 4;           // 1 KB (four-row) DMA blocks per K or V tile
 constexpr int WAVE_BLOCKS = BLOCKS / WAVES;   // K (and V) blocks copied by each wave
 constexpr float kRescaleLog2 = 8.0f;     // move the running max when it grows by > 2^8
