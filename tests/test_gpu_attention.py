@@ -42,9 +42,11 @@ def test_workload_stages(cfg, stage):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("kv_split", [64, 128, 320])
+@pytest.mark.parametrize("kv_split", [64, 128, 320, 512])
 def test_split_reduction(dtype, kv_split):
-    """Many context splits with a ragged last split exercise the LSE reduction."""
+    """Many context splits with a ragged last split exercise the LSE reduction
+    (four or more splits in the longest context: the four-group merge; two:
+    the one-group merge)."""
     lay = wl.custom_layout(16, [[3, 7], [1], [], [2, 5, 9, 15]], [1000, 129, 64, 1], hq=8, hkv=2,
                            dtype=dtype, seed=11)
     check_full(Case(lay), "cascade", kv_split)
