@@ -8,9 +8,12 @@ attention -> accept path, on a seeded synthetic batch resident in HBM.
     python bench.py --copy-probe       (HBM counter calibration copy)
 
 Prints one JSON line. value = verified tree tokens per second of the whole
-step (tree nodes verified / step time). The roofline object describes the
-cascade attention kernel (the step's dominant kernel), timed with HIP events
-recorded by the library on its launch stream over the timed steps.
+step (tree nodes verified / step time, K steps back to back). The roofline
+object describes the cascade attention kernel (the step's dominant kernel),
+timed with HIP events recorded by the library on its launch stream over the
+timed steps. `timing` adds per-step median / p10 / p90 of the step and of the
+attention kernel, warm (back to back) and cold (each step after a 512 MiB
+write that evicts every cache level).
 """
 
 from __future__ import annotations
@@ -30,6 +33,14 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix peaks
 METRIC = "verified tree tokens/sec + prefix-KV HBM GB/s (% of peak), cascade verify attn"
+FLUSH_BYTES = 512 << 20         # larger than the 256 MB Infinity Cache and every L2
+
+
+def percentiles(v) -> dict:
+    """Median, 10th and 90th percentile of a list of times (ms)."""
+    a = np.asarray(v, np.float64)
+    return {"median": round(float(np.median(a)), 4), "p10": round(float(np.percentile(a, 10)), 4),
+            "p90": round(float(np.percentile(a, 90)), 4)}
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_04446_amd", "csrc", f) for f in ("attention.hip", "common.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cascade_attention_traffic.json")
 
@@ -293,6 +304,34 @@ def main():
     launches, kern_ms_total = d2sd.kernel_timing_collect()
     kern_ms = kern_ms_total / max(launches, 1)
 
+    # Per-step distributions, outside the timed bracket above: the steps run
+    # back to back as there, with an event pair around each step and the
+    # library's events around each attention launch. "warm": nothing between
+    # steps; "cold": a 512 MiB write before every step evicts the L2 caches
+    # and the 256 MB Infinity Cache, so every input is read from HBM.
+    flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+
+    def per_step(reps, flush):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_collect_each()
+        d2sd.kernel_timing_enable(True)
+        for i, (e_a, e_b) in enumerate(evs):
+            if flush:
+                flush_buf.fill_(i & 0xff)
+            e_a.record()
+            step()
+            e_b.record()
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_enable(False)
+        attn_t = d2sd.kernel_timing_collect_each()
+        return {"step_ms": percentiles([e_a.elapsed_time(e_b) for e_a, e_b in evs]),
+                "attn_ms": percentiles(attn_t)}
+
+    timing = {"reps": args.steps, "warm": per_step(args.steps, False), "cold": per_step(args.steps, True),
+              "flush_bytes": FLUSH_BYTES}
+    del flush_buf
+
     # The same step captured once in a HIP graph and replayed: the four
     # launches of a step then cost one graph launch (the step allocates
     # nothing and issues no memset, so it can be captured as it is).
@@ -367,6 +406,7 @@ def main():
         "attn_tokens_per_s": round(total / t_s, 1),
         "kernel_sha": kernel_sha(),
         "requested_kv_split": args.kv_split,
+        "timing": timing,
     }
     if args.noncascade:
         out2 = torch.empty_like(out)

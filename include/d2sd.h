@@ -418,6 +418,14 @@ d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head
 d2sd_status d2sd_kernel_timing_enable(int enable);
 d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms);
 
+/*
+ * Host. As d2sd_kernel_timing_collect, but writes the duration of each
+ * recorded launch (milliseconds, launch order) to ms_each[0 .. min(n,
+ * capacity)) (host memory, caller-owned) and the launch count n to
+ * *launches; durations past capacity are dropped. Clears the record.
+ */
+d2sd_status d2sd_kernel_timing_collect_each(int capacity, float* ms_each, int* launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -66,6 +66,31 @@ void timing_begin(hipEvent_t* e0, hipEvent_t* e1) {
   g_timing_pending.emplace_back(*e0, *e1);
 }
 
+// Wait for every recorded event pair, return each duration (ms) in launch
+// order, recycle the events and clear the record.
+hipError_t collect_timings(std::vector<float>* each) {
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pend;
+  {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    pend.swap(g_timing_pending);
+  }
+  hipError_t err = hipSuccess;
+  each->reserve(pend.size());
+  for (auto& pr : pend) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(pr.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+    each->push_back(ms);
+  }
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  for (auto& pr : pend) {
+    g_event_pool.push_back(pr.first);
+    g_event_pool.push_back(pr.second);
+  }
+  return err;
+}
+
 // Largest tree any entry point accepts: the canonical tree of B = D2SD_MAX_B
 // with every re-anchor position (the accept kernel stages one tree in LDS).
 constexpr int kMaxTreeNodes = D2SD_MAX_B + D2SD_MAX_B * (D2SD_MAX_B - 1) / 2;
@@ -423,29 +448,22 @@ d2sd_status d2sd_kernel_timing_enable(int enable) {
 
 d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms) {
   if (!launches || !total_ms) return fail(D2SD_ERR_INVALID_ARG, "output pointer is NULL");
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> pend;
-  {
-    std::lock_guard<std::mutex> lk(g_timing_mu);
-    pend.swap(g_timing_pending);
-  }
+  std::vector<float> each;
+  const hipError_t err = collect_timings(&each);
   double sum = 0.0;
-  hipError_t err = hipSuccess;
-  for (auto& pr : pend) {
-    float ms = 0.0f;
-    hipError_t e = hipEventSynchronize(pr.second);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
-    if (e != hipSuccess && err == hipSuccess) err = e;
-    sum += ms;
-  }
-  {
-    std::lock_guard<std::mutex> lk(g_timing_mu);
-    for (auto& pr : pend) {
-      g_event_pool.push_back(pr.first);
-      g_event_pool.push_back(pr.second);
-    }
-  }
-  *launches = (int)pend.size();
+  for (float ms : each) sum += ms;
+  *launches = (int)each.size();
   *total_ms = sum;
+  return hip_status(err, "kernel timing");
+}
+
+d2sd_status d2sd_kernel_timing_collect_each(int capacity, float* ms_each, int* launches) {
+  if (!launches || capacity < 0 || (capacity > 0 && !ms_each))
+    return fail(D2SD_ERR_INVALID_ARG, "launches is NULL, capacity < 0, or ms_each is NULL");
+  std::vector<float> each;
+  const hipError_t err = collect_timings(&each);
+  for (size_t i = 0; i < each.size() && i < (size_t)capacity; ++i) ms_each[i] = each[i];
+  *launches = (int)each.size();
   return hip_status(err, "kernel timing");
 }
 

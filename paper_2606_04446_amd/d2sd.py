@@ -90,6 +90,7 @@ _sample = _sig("d2sd_sample_targets", _c_int, _c_int, _c_ptr, _c_int, _c_int, _c
                 ctypes.c_float, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _timing_enable = _sig("d2sd_kernel_timing_enable", _c_int, _c_int)
 _timing_collect = _sig("d2sd_kernel_timing_collect", _c_int, _c_int_p, ctypes.POINTER(ctypes.c_double))
+_timing_each = _sig("d2sd_kernel_timing_collect_each", _c_int, _c_int, ctypes.POINTER(ctypes.c_float), _c_int_p)
 
 
 def _check(status: int, where: str):
@@ -422,3 +423,11 @@ def kernel_timing_collect():
     ms = ctypes.c_double(0.0)
     _check(_timing_collect(ctypes.byref(n), ctypes.byref(ms)), "d2sd_kernel_timing_collect")
     return n.value, ms.value
+
+
+def kernel_timing_collect_each(capacity: int = 4096):
+    """Durations (ms, launch order) of the context-streaming kernel since the last collect."""
+    buf = (ctypes.c_float * capacity)()
+    n = ctypes.c_int(0)
+    _check(_timing_each(capacity, buf, ctypes.byref(n)), "d2sd_kernel_timing_collect_each")
+    return [float(buf[i]) for i in range(min(n.value, capacity))]

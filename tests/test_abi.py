@@ -235,3 +235,9 @@ def test_noncascade_validation():
 def test_timing_collect_empty():
     d2sd.kernel_timing_enable(False)
     assert d2sd.kernel_timing_collect() == (0, 0.0)
+    assert d2sd.kernel_timing_collect_each() == []
+    n = ctypes.c_int(-1)
+    assert d2sd._timing_each(0, None, ctypes.byref(n)) == d2sd.OK and n.value == 0
+    assert d2sd._timing_each(-1, None, ctypes.byref(n)) == d2sd.ERR_INVALID_ARG
+    assert d2sd._timing_each(4, None, ctypes.byref(n)) == d2sd.ERR_INVALID_ARG
+    assert d2sd._timing_each(0, None, None) == d2sd.ERR_INVALID_ARG
