@@ -332,6 +332,26 @@ def main():
               "flush_bytes": FLUSH_BYTES}
     del flush_buf
 
+    # The prefix stage alone (context keys only, no tree tiles): the time
+    # that the prefix K/V bandwidth is quoted against, beside the whole
+    # attention call.
+    out_p, lse_p = torch.empty_like(out), torch.empty_like(lse)
+    prefix_call = lambda: d2sd.cascade_verify_attention(
+        x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"], d_ip, tree["anc_mask"],
+        total_nodes=total, max_nodes=max_nodes, max_ctx_len=max_ctx, stage=d2sd.STAGE_PREFIX,
+        kv_split=args.kv_split, out=out_p, lse=lse_p, workspace=ws)
+    for _ in range(args.warmup):
+        prefix_call()
+    torch.cuda.synchronize()
+    d2sd.kernel_timing_collect_each()
+    d2sd.kernel_timing_enable(True)
+    for _ in range(args.steps):
+        prefix_call()
+    torch.cuda.synchronize()
+    d2sd.kernel_timing_enable(False)
+    prefix_ms = float(np.mean(d2sd.kernel_timing_collect_each()))
+    del out_p, lse_p
+
     # The same step captured once in a HIP graph and replayed: the four
     # launches of a step then cost one graph launch (the step allocates
     # nothing and issues no memset, so it can be captured as it is).
@@ -400,6 +420,9 @@ def main():
         "roofline": roof,
         "prefix_kv_gbps": round(gbps, 1),
         "prefix_kv_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "prefix_stage": {"kernel_ms": round(prefix_ms, 4),
+                         "prefix_kv_gbps": round(prefix_bytes / (prefix_ms / 1e3) / 1e9, 1),
+                         "prefix_kv_hbm_frac": round(prefix_bytes / (prefix_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)},
         "attn_tflops": round(tflops, 2),
         "attn_mfma_frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4),
         "attn_kernel_ms": round(kern_ms, 4),
