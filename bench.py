@@ -196,24 +196,37 @@ def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float, parents=N
         q = x["q"][s:e].float().cpu().numpy()
         kt = x["k_tree"][s:e].float().cpu().numpy()
         vt = x["v_tree"][s:e].float().cpu().numpy()
+        def run_oracle():
+            tree = (build_tree(layout.spec.B, layout.p[b, :layout.K[b]]) if parents is None
+                    else tree_from_parents(parents[b], layout.spec.B))
+            kcb, vcb = gather_context(kc, vc, np.arange(npg), C, 16)
+            request_attention(q.astype(np.float64), kcb, vcb, kt.astype(np.float64), vt.astype(np.float64), tree)
+
         t0 = time.perf_counter()
-        tree = (build_tree(layout.spec.B, layout.p[b, :layout.K[b]]) if parents is None
-                else tree_from_parents(parents[b], layout.spec.B))
-        kcb, vcb = gather_context(kc, vc, np.arange(npg), C, 16)
-        request_attention(q.astype(np.float64), kcb, vcb, kt.astype(np.float64), vt.astype(np.float64), tree)
+        run_oracle()
         t_total += time.perf_counter() - t0
         done_nodes += e - s
         done_req += 1
+        if layout.batch == 1:
+            # a single request: the same oracle call with one BLAS thread
+            from threadpoolctl import threadpool_limits
+            with threadpool_limits(limits=1):
+                t1 = time.perf_counter()
+                run_oracle()
+                one_thread = (e - s) / (time.perf_counter() - t1)
         if t_total >= budget_s:
             break
     blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
     cores = max(blas) if blas else 1
-    return {
+    res = {
         "value": done_nodes / t_total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
         "sample": f"{done_req} of {layout.batch} requests (tree build + float64 attention of every node "
                   f"and query head over the full context and its ancestors), {t_total:.1f} s, "
                   f"{len(os.sched_getaffinity(0))} host cores visible",
     }
+    if layout.batch == 1:
+        res["value_1_thread"] = one_thread
+    return res
 
 
 def main():
