@@ -131,6 +131,27 @@ def test_deterministic():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_kernel_timing_per_launch():
+    """The library's launch-stream events: one duration per attention launch,
+    in launch order, cleared by the read; nothing is recorded while off."""
+    m = d2sd()
+    case = Case(wl.draw_layout(2))
+    case.attention()
+    torch.cuda.synchronize()
+    m.kernel_timing_collect_each()
+    m.kernel_timing_enable(True)
+    for _ in range(3):
+        case.attention()
+    torch.cuda.synchronize()
+    m.kernel_timing_enable(False)
+    each = m.kernel_timing_collect_each()
+    assert len(each) == 3 and all(0.0 < ms < 1000.0 for ms in each)
+    assert m.kernel_timing_collect_each() == []
+    case.attention()
+    torch.cuda.synchronize()
+    assert m.kernel_timing_collect() == (0, 0.0)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_noncascade_baseline(dtype):
     lay = wl.custom_layout(16, [[3, 7], [], [1, 2, 3, 4]], [500, 64, 33], hq=8, hkv=2, dtype=dtype, seed=16)
