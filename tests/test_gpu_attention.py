@@ -76,6 +76,24 @@ def test_contexts_longer_than_one_split(dtype):
     check_full(case, "cascade", kv_split=32768)
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_random_layouts(seed):
+    """Seeded random batches: block length, re-anchor sets, context lengths
+    (page- and tile-ragged, some empty), head grouping, dtype and split
+    length all drawn, then every output row against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    B = int(rng.choice([2, 3, 5, 8, 13, 16, 24, 32]))
+    batch = int(rng.integers(1, 6))
+    rows = [sorted(rng.choice(np.arange(1, B), int(rng.integers(0, B)), replace=False).tolist())
+            for _ in range(batch)]
+    ctx = [int(c) for c in rng.choice([0, 1, 15, 16, 17, 31, 33, 100, 257, 1000, 2049, 3000], batch)]
+    hq, hkv = [(4, 1), (8, 2), (16, 4), (32, 8), (12, 3), (8, 8)][int(rng.integers(0, 6))]
+    dtype = "f32" if seed % 4 == 3 else "bf16"
+    kv_split = int(rng.choice([0, 64, 256, 1024]))
+    lay = wl.custom_layout(B, rows, ctx, hq=hq, hkv=hkv, dtype=dtype, seed=seed)
+    check_full(Case(lay, poison_slack=True), "cascade", kv_split)
+
+
 @pytest.mark.parametrize("hq,hkv", [(8, 8), (12, 4), (64, 8), (6, 1)])
 def test_gqa_groupings(hq, hkv):
     lay = wl.custom_layout(16, [[2, 9], [5, 6, 7, 8]], [200, 77], hq=hq, hkv=hkv, dtype="bf16", seed=13)
