@@ -537,11 +537,27 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     draw_s = e0.elapsed_time(e1) / 1e3 / args.steps
+    # cold: each draw after a 512 MiB write, so the logits come from HBM and
+    # not from the Infinity Cache, which holds the whole batch's rows when
+    # they fit (167 MB on the bench workload)
+    flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i, (e_a, e_b) in enumerate(evs):
+        flush_buf.fill_(i & 0xff)
+        e_a.record()
+        draw()
+        e_b.record()
+    torch.cuda.synchronize()
+    cold_s = float(np.median([e_a.elapsed_time(e_b) for e_a, e_b in evs])) / 1e3
+    del flush_buf
     acc_t = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, toks)
     draw_bytes = total * Vs * 2                            # every node streams one logits row once
     draw_gbps = draw_bytes / draw_s / 1e9
+    cold_gbps = draw_bytes / cold_s / 1e9
     res["sampling"] = {"temperature": args.temperature, "vocab": Vs, "rows": total, "us": round(draw_s * 1e6, 2),
                        "gbps": round(draw_gbps, 1), "hbm_frac": round(draw_gbps / HBM_PEAK_GBPS, 4),
+                       "us_cold": round(cold_s * 1e6, 2), "gbps_cold": round(cold_gbps, 1),
+                       "hbm_frac_cold": round(cold_gbps / HBM_PEAK_GBPS, 4),
                        "mean_accept_len": round(float(acc_t["accept_len"].float().mean()), 3),
                        "greedy_mean_accept_len": round(float(acc["accept_len"].float().mean()), 3)}
     del logits
