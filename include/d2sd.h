@@ -176,7 +176,10 @@ d2sd_status d2sd_tree_from_parents(int batch, const int* node_indptr, int total_
  * operations), so the result is reproducible bit for bit. The min(K[b], Kmax,
  * B-1) largest r(i) are kept, equal values going to the smaller i; prefix
  * length i gives the re-anchor position p = i + 1.
- *  conf[batch, B-1]  float32, conf[b, k-1] = c_k in [0, 1] (not checked).
+ *  conf[batch, B-1]  float32, conf[b, k-1] = c_k in [0, 1] (not checked; a
+ *                    NaN r(i) ranks below every number, so exactly
+ *                    min(K[b], Kmax, B-1) positions are written whatever
+ *                    the values).
  *  K[batch]          int32 branch counts (clamped to [0, min(Kmax, B-1)]).
  *  p_out[batch, Kmax] int32 out: the kept positions in ascending order, then
  *                    -1 up to Kmax. Feeds d2sd_tree_indptr / d2sd_tree_build.

@@ -11,6 +11,8 @@ re-anchor block position p = i + 1.
 
 from __future__ import annotations
 
+import math
+
 
 def rejection_posterior(conf) -> list:
     """r(0..gamma-2) from confidences c_1..c_{gamma-1} (conf[0] is c_1)."""
@@ -25,8 +27,14 @@ def rejection_posterior(conf) -> list:
 
 
 def top_k_prefixes(r, K: int) -> list:
-    """Indices i of the K largest r(i); ties go to the smaller i."""
-    order = sorted(range(len(r)), key=lambda i: (-r[i], i))
+    """Indices i of the K largest r(i); ties go to the smaller i.
+
+    The paper assumes confidences in [0, 1]. Outside that range r(i) can be
+    NaN; such an r(i) is read as the least likely prefix length (it ranks
+    below every number, -inf included, ties again by index)."""
+    def rank_key(i):
+        return (math.inf if math.isnan(r[i]) else -r[i], i)
+    order = sorted(range(len(r)), key=rank_key)
     return sorted(order[:K])
 
 

@@ -34,7 +34,11 @@ __global__ __launch_bounds__(kSelectThreads) void select_reanchor_kernel(
   const int n = B - 1;                 // number of prefix lengths 0..B-2
   const float* c = conf + (size_t)b * n;
   const double r = i < n ? posterior(c, i) : 0.0;
-  s_r[i] = r;
+  // Ranking key: a NaN posterior (from confidences outside [0, 1] or NaN)
+  // ranks below every number, so the order stays total and exactly Kb
+  // prefix lengths are kept.
+  const double key = __builtin_isnan(r) ? -INFINITY : r;
+  s_r[i] = key;
   __syncthreads();
   const int Kb = clampi(K[b], 0, min(Kmax, n));
   bool keep = false;
@@ -42,7 +46,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_reanchor_kernel(
     int rank = 0;                       // prefix lengths ordered before i
     for (int j = 0; j < n; ++j) {
       const double rj = s_r[j];
-      rank += (rj > r) || (rj == r && j < i);
+      rank += (rj > key) || (rj == key && j < i);
     }
     keep = rank < Kb;
     if (r_out) r_out[(size_t)b * n + i] = r;
@@ -51,7 +55,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_reanchor_kernel(
   const uint64_t kept = __ballot(keep);
   if (keep) {
     const int slot = __popcll(kept & ((1ull << i) - 1ull));
-    p_out[(size_t)b * Kmax + slot] = i + 1;
+    if (slot < Kb) p_out[(size_t)b * Kmax + slot] = i + 1;
   }
   for (int k = Kb + i; k < Kmax; k += kSelectThreads) p_out[(size_t)b * Kmax + k] = -1;
 }

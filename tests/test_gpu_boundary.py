@@ -31,6 +31,8 @@ def draw_conf(rng, kind, batch, n):
         c = rng.choice([0.0, 0.25, 0.5, 0.75, 1.0], size=(batch, n))
     elif kind == "extreme":
         c = rng.choice([0.0, 1.0, 1e-30, 1.0 - 2 ** -24], size=(batch, n))
+    elif kind == "invalid":       # outside [0, 1]: NaN and +-inf posteriors
+        c = rng.choice([np.nan, np.inf, -np.inf, -0.5, 1.5, 0.0, 0.3, 0.7, 1.0], size=(batch, n))
     else:
         raise ValueError(kind)
     return c.astype(np.float32)
@@ -49,13 +51,13 @@ def check_select(B, Kmax, kind, seed, batch=64):
     p, r = p.cpu().numpy(), r.cpu().numpy()
     for b in range(batch):
         r_or = np.array(rejection_posterior(conf[b]), dtype=np.float64)
-        assert np.array_equal(r[b], r_or), (B, kind, b, r[b], r_or)
+        assert np.array_equal(r[b], r_or, equal_nan=True), (B, kind, b, r[b], r_or)
         want = reanchor_positions(conf[b], int(K[b]))
         got = p[b].tolist()
         assert got == want + [-1] * (Kmax - len(want)), (B, kind, b, got, want)
 
 
-@pytest.mark.parametrize("kind", ["uniform", "beta52", "constant", "quantized", "extreme"])
+@pytest.mark.parametrize("kind", ["uniform", "beta52", "constant", "quantized", "extreme", "invalid"])
 @pytest.mark.parametrize("B", [2, 3, 4, 16, 33, 64])
 def test_select_reanchor_matches_oracle(B, kind):
     check_select(B, max(1, min(8, B - 1)), kind, seed=7)
@@ -65,6 +67,26 @@ def test_select_reanchor_full_and_wide_kmax():
     check_select(16, 15, "beta52", seed=1)      # K up to B - 1 (every position)
     check_select(16, 40, "uniform", seed=2)     # Kmax above B - 1: rows padded with -1
     check_select(64, 63, "quantized", seed=3)
+
+
+@pytest.mark.parametrize("B", [4, 16, 64])
+def test_select_reanchor_invalid_confidences_stay_in_bounds(B):
+    """NaN posteriors rank last (the oracle's reading), so exactly K positions
+    are written per request: a guard region after p_out stays untouched."""
+    m = d2sd()
+    rng = np.random.default_rng([11, B])
+    batch, Kmax, guard = 32, 3, 256
+    conf = draw_conf(rng, "invalid", batch, B - 1)
+    K = np.full(batch, min(Kmax, B - 1), dtype=np.int32)
+    dev = torch.device("cuda")
+    buf = torch.full((batch * Kmax + guard,), -7, dtype=torch.int32, device=dev)
+    p_out = buf[:batch * Kmax].view(batch, Kmax)
+    p, _ = m.select_reanchor(B, torch.from_numpy(conf).to(dev), torch.from_numpy(K).to(dev), Kmax, p_out=p_out)
+    torch.cuda.synchronize()
+    assert (buf[batch * Kmax:] == -7).all().item()
+    got = p.cpu().numpy()
+    for b in range(batch):
+        assert got[b].tolist() == reanchor_positions(conf[b], int(K[b])), (B, b, conf[b], got[b])
 
 
 def test_select_reanchor_clamps_k():

@@ -38,3 +38,18 @@ def test_constant_confidence_is_geometric():
 def test_ties_go_to_smaller_prefix():
     assert top_k_prefixes([0.2, 0.3, 0.3, 0.2], 1) == [1]
     assert top_k_prefixes([0.2, 0.3, 0.3, 0.2], 3) == [0, 1, 2]
+
+
+def test_nan_posterior_ranks_last():
+    # confidences outside [0, 1]: 0 * (1 - inf) and 0 * inf are NaN, and
+    # 0.5 * (1 - inf) is -inf
+    r = rejection_posterior([0.0, float("inf"), 0.5])
+    assert r[0] == 1.0 and np.isnan(r[1]) and np.isnan(r[2])
+    assert top_k_prefixes(r, 2) == [0, 1]
+    r = rejection_posterior([0.5, float("inf"), 0.5])
+    assert r[:2] == [0.5, -float("inf")] and r[2] == float("inf")
+    nan = float("nan")
+    assert top_k_prefixes([nan, 0.1, nan, 0.3], 2) == [1, 3]
+    assert top_k_prefixes([nan, 0.1, nan, 0.3], 3) == [0, 1, 3]      # first NaN by index
+    assert top_k_prefixes([nan, -float("inf"), nan], 2) == [0, 1]     # -inf ranks above NaN
+    assert top_k_prefixes([nan] * 4, 4) == [0, 1, 2, 3]
