@@ -72,6 +72,40 @@ def test_tree_plan_rejects(B, K, p, msg):
     assert (out == -7).all()          # outputs untouched on error
 
 
+def test_tree_plan_validation_agrees_with_oracle():
+    """Random (B, K, p), valid or not: the host plan accepts exactly the inputs
+    the oracle's validation accepts (B <= 64 on top), with its node counts."""
+    from oracle.tree import validate
+    rng = np.random.default_rng(21)
+    accepted = rejected = 0
+    for _ in range(400):
+        B = int(rng.integers(0, 68))
+        batch = int(rng.integers(1, 5))
+        kmax = int(rng.integers(1, 8))
+        K = rng.integers(-1, kmax + 2, size=batch).astype(np.int32)
+        p = rng.integers(-1, max(B, 1) + 2, size=(batch, kmax)).astype(np.int32)
+        ok = 2 <= B <= 64 and all(0 <= K[b] <= kmax for b in range(batch))
+        counts = []
+        for b in range(batch):
+            if not ok:
+                break
+            try:
+                counts.append(build_tree(B, validate(B, p[b, :K[b]].tolist())).N)
+            except ValueError:
+                ok = False
+        out = np.full(batch + 1, -7, np.int32)
+        st = lib.d2sd_tree_plan(batch, B, K.ctypes.data, p.ctypes.data, kmax, out.ctypes.data, None)
+        if ok:
+            accepted += 1
+            assert st == d2sd.OK, (B, K, p, d2sd.last_error())
+            assert out.tolist() == np.concatenate([[0], np.cumsum(counts)]).tolist()
+        else:
+            rejected += 1
+            assert st == d2sd.ERR_INVALID_ARG, (B, K, p)
+            assert (out == -7).all()
+    assert accepted > 40 and rejected > 40
+
+
 def test_tree_plan_null_pointer():
     K = np.zeros(1, np.int32)
     assert lib.d2sd_tree_plan(1, 4, K.ctypes.data, None, 0, None, None) == d2sd.ERR_INVALID_ARG
