@@ -399,8 +399,10 @@ d2sd_status d2sd_sample_targets(int batch, const int* node_indptr, int total_nod
  *  ctx_len[batch]: in/out (device). Values are clamped to [0, max_ctx_len].
  *  k_cache, v_cache [num_pages, num_kv_heads, page_size, head_dim]: out.
  * head_dim = D2SD_HEAD_DIM, page_size = D2SD_PAGE_SIZE, dtype D2SD_F32 or
- * D2SD_BF16; max_ctx_len + B <= max_pages * page_size. Must not run
- * concurrently with an attention call reading the same cache or ctx_len.
+ * D2SD_BF16; max_ctx_len + B <= max_pages * page_size;
+ * B * num_kv_heads * head_dim * sizeof(dtype) / 16 <= 2^31 - 1. Entries of
+ * path_nodes outside [0, total_nodes - node_indptr[b]) are skipped. Must not
+ * run concurrently with an attention call reading the same cache or ctx_len.
  * Errors: INVALID_ARG / UNSUPPORTED before any launch.
  */
 d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head_dim, int page_size, int dtype,

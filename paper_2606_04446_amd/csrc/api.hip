@@ -325,6 +325,8 @@ d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head
       !v_cache)
     return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
   const int row_bytes = head_dim * (dtype == D2SD_BF16 ? 2 : 4);
+  if ((long long)B * num_kv_heads * (row_bytes / 16) > 0x7fffffffll)
+    return fail(D2SD_ERR_UNSUPPORTED, "B x num_kv_heads x %d chunks exceeds 2^31 - 1", row_bytes / 16);
   return hip_status(d2sd::launch_commit(batch, B, num_kv_heads, row_bytes, num_pages, max_pages, max_ctx_len,
                                         node_indptr, total_nodes, path_nodes, accept_len, k_tree, v_tree,
                                         page_table, ctx_len, k_cache, v_cache, stream),

@@ -36,8 +36,8 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(
     const int h = rem / row_chunks;
     const int c = rem - h * row_chunks;
     const int local = path_nodes[(size_t)b * B + d];
+    if (local < 0 || local >= total_nodes - base) continue;   // no overflow: base <= total_nodes
     const int node = base + local;
-    if (local < 0 || node >= total_nodes) continue;
     const int pos = C + d;
     const int page = clampi(page_table[(size_t)b * max_pages + pos / D2SD_PAGE_SIZE], 0, num_pages - 1);
     const size_t dst = (((size_t)page * hkv + h) * D2SD_PAGE_SIZE + pos % D2SD_PAGE_SIZE) * row_chunks + c;

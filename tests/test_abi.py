@@ -155,6 +155,8 @@ def test_commit_validation():
     assert call(P=32) == d2sd.ERR_UNSUPPORTED
     assert call(dt=5) == d2sd.ERR_INVALID_ARG
     assert call(maxc=64 * 16 - 15) == d2sd.ERR_INVALID_ARG     # positions up to C + B must have pages
+    assert call(hkv=1 << 26) == d2sd.ERR_UNSUPPORTED             # chunk index of a path past 2^31
+    assert "exceeds" in d2sd.last_error()
     assert c(1, 16, 8, 128, 16, d2sd.BF16, 64, 64, 100, f, 10, f, f, f, f, f, None, f, f, None) == d2sd.ERR_INVALID_ARG
 
 

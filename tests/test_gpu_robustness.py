@@ -1,0 +1,173 @@
+"""Device arrays that disagree with the host-side sizes.
+
+The header promises that node offsets, context lengths, page ids, parents,
+depths, path nodes and accepted lengths read from device memory are clamped
+or skipped inside the kernels, so that no access leaves the buffers the
+host-side sizes describe (the results are then undefined). Every case here
+runs an entry point on such arrays, with every output buffer followed by a
+guard region that must come back untouched, and then checks that inputs the
+call does not own are unchanged and that a valid call still gives the same
+result as before.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_04446_amd import workload as wl
+from tests.gpu_cases import Case
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 4096
+INT_MIN, INT_MAX = -(1 << 31), (1 << 31) - 1
+
+
+def d2sd():
+    from paper_2606_04446_amd import d2sd as m
+    return m
+
+
+def guarded(shape, dtype, fill):
+    """A contiguous tensor of `shape` followed by GUARD elements of `fill`."""
+    n = int(np.prod(shape))
+    buf = torch.full((n + GUARD,), fill, dtype=dtype, device="cuda")
+    return buf, buf[:n].view(shape)
+
+
+def guard_intact(buf, shape, fill):
+    n = int(np.prod(shape))
+    return bool((buf[n:] == fill).all().item())
+
+
+def garbage_i32(rng, n):
+    """int32 values mixing the extremes, negatives and plausible indices."""
+    pool = np.array([INT_MIN, INT_MIN + 1, -(1 << 30), -1, 0, 1, 7, 1 << 20, 1 << 30, INT_MAX], np.int64)
+    v = np.where(rng.random(n) < 0.5, rng.choice(pool, n), rng.integers(INT_MIN, INT_MAX, n, endpoint=True))
+    return torch.from_numpy(v.astype(np.int32)).cuda()
+
+
+def small_case(dtype):
+    lay = wl.custom_layout(16, [[3, 7], [2], [], [5, 9, 12]], [100, 40, 0, 257], hq=8, hkv=2, dtype=dtype, seed=3)
+    return Case(lay)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_attention_with_inconsistent_offsets_lengths_and_pages(dtype):
+    m = d2sd()
+    c = small_case(dtype)
+    x = c.x
+    rng = np.random.default_rng([5, int(dtype == "bf16")])
+    batch = c.layout.batch
+    max_ctx = int(c.layout.ctx_len.max())
+    ref, ref_lse = c.attention(kv_split=64)
+    torch.cuda.synchronize()
+    inputs = {k: v.clone() for k, v in x.items()}
+    bad_ip = garbage_i32(rng, batch + 1)
+    bad_ctx = garbage_i32(rng, batch)
+    bad_pt = garbage_i32(rng, c.d_pt.numel()).view_as(c.d_pt)
+    for kv_split in (64, 0):
+        obuf, out = guarded(tuple(x["q"].shape), x["q"].dtype, 7.0)
+        lbuf, lse = guarded(tuple(x["q"].shape[:2]), torch.float32, 7.0)
+        a = m.attn_args(x["q"], x["k_cache"], x["v_cache"], bad_pt, bad_ctx, x["k_tree"], x["v_tree"], bad_ip,
+                        c.tree["anc_mask"], out, lse, total_nodes=c.total, max_nodes=c.max_nodes,
+                        max_ctx_len=max_ctx, kv_split=kv_split)
+        need = m.cascade_workspace_size(a)
+        wbuf, ws = guarded((max(need, 1),), torch.uint8, 0x5A)
+        m.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], bad_pt, bad_ctx, x["k_tree"], x["v_tree"],
+                                   bad_ip, c.tree["anc_mask"], total_nodes=c.total, max_nodes=c.max_nodes,
+                                   max_ctx_len=max_ctx, kv_split=kv_split, out=out, lse=lse, workspace=ws)
+        torch.cuda.synchronize()
+        assert guard_intact(obuf, out.shape, 7.0) and guard_intact(lbuf, lse.shape, 7.0)
+        assert guard_intact(wbuf, ws.shape, 0x5A)
+    obuf, out = guarded(tuple(x["q"].shape), x["q"].dtype, 7.0)
+    m.noncascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], bad_pt, bad_ctx, x["k_tree"], x["v_tree"],
+                                  bad_ip, c.tree["anc_mask"], total_nodes=c.total, max_nodes=c.max_nodes,
+                                  max_ctx_len=max_ctx, out=out)
+    torch.cuda.synchronize()
+    assert guard_intact(obuf, out.shape, 7.0)
+    for k, v in inputs.items():
+        assert torch.equal(x[k], v), k
+    again, again_lse = c.attention(kv_split=64)
+    torch.cuda.synchronize()
+    assert torch.equal(again, ref) and torch.equal(again_lse, ref_lse)
+
+
+def test_tree_kernels_with_inconsistent_inputs():
+    m = d2sd()
+    rng = np.random.default_rng(6)
+    B, batch, kmax = 16, 5, 4
+    W = m.mask_words(B)
+    total = 160
+    bad_ip = garbage_i32(rng, batch + 1)
+    bufs = {}
+    out = {}
+    for name, shape in (("parent", (total,)), ("depth", (total,)), ("path_id", (total,)),
+                        ("anc_mask", (total, W)), ("path_leaf", (batch, kmax + 1))):
+        bufs[name], out[name] = guarded(shape, torch.int32, -7)
+    m.tree_build(B, garbage_i32(rng, batch), garbage_i32(rng, batch * kmax).view(batch, kmax), bad_ip, total, W,
+                 out=out)
+    torch.cuda.synchronize()
+    for name in bufs:
+        assert guard_intact(bufs[name], out[name].shape, -7), name
+    max_nodes, W2 = 64, 2
+    bufs, out = {}, {}
+    for name, shape in (("depth", (total,)), ("path_id", (total,)), ("anc_mask", (total, W2))):
+        bufs[name], out[name] = guarded(shape, torch.int32, -7)
+    m.tree_from_parents(bad_ip, total, max_nodes, garbage_i32(rng, total), W2, out=out)
+    torch.cuda.synchronize()
+    for name in bufs:
+        assert guard_intact(bufs[name], out[name].shape, -7), name
+    ibuf, ip = guarded((batch + 1,), torch.int32, -7)
+    m.tree_indptr(B, garbage_i32(rng, batch), garbage_i32(rng, batch * kmax).view(batch, kmax), out=ip)
+    torch.cuda.synchronize()
+    assert guard_intact(ibuf, ip.shape, -7)
+
+
+def test_accept_and_commit_with_inconsistent_inputs():
+    m = d2sd()
+    rng = np.random.default_rng(7)
+    B, batch, total = 16, 6, 200
+    bad_ip = garbage_i32(rng, batch + 1)
+    bufs, out = {}, {}
+    for name, shape in (("accept_len", (batch,)), ("best_path", (batch,)), ("accept_node", (batch,)),
+                        ("path_nodes", (batch, B)), ("out_tokens", (batch, B))):
+        bufs[name], out[name] = guarded(shape, torch.int32, -7)
+    res = m.accept_path(B, bad_ip, total, garbage_i32(rng, total), garbage_i32(rng, total),
+                        garbage_i32(rng, total), garbage_i32(rng, total), garbage_i32(rng, total), out=out)
+    torch.cuda.synchronize()
+    for name in bufs:
+        assert guard_intact(bufs[name], out[name].shape, -7), name
+    L = res["accept_len"].cpu().numpy()
+    assert ((L >= 0) & (L <= B - 1)).all()
+
+    hkv, P, D, num_pages, max_pages, max_ctx = 2, 16, 128, 40, 8, 100
+    kbuf, k_cache = guarded((num_pages, hkv, P, D), torch.bfloat16, 3.0)
+    vbuf, v_cache = guarded((num_pages, hkv, P, D), torch.bfloat16, 3.0)
+    k_tree = torch.randn(total, hkv, D, device="cuda").to(torch.bfloat16)
+    v_tree = torch.randn(total, hkv, D, device="cuda").to(torch.bfloat16)
+    cbuf, ctx = guarded((batch,), torch.int32, -7)
+    ctx.copy_(garbage_i32(rng, batch))
+    path_nodes = garbage_i32(rng, batch * B).view(batch, B)
+    path_nodes[0, :] = INT_MAX                                # base + local would overflow int32
+    m.commit_accepted_kv(B, bad_ip, total, path_nodes, garbage_i32(rng, batch), k_tree, v_tree,
+                         garbage_i32(rng, batch * max_pages).view(batch, max_pages), ctx, k_cache, v_cache, max_ctx)
+    torch.cuda.synchronize()
+    assert guard_intact(kbuf, k_cache.shape, 3.0) and guard_intact(vbuf, v_cache.shape, 3.0)
+    assert guard_intact(cbuf, ctx.shape, -7)
+
+
+@pytest.mark.parametrize("temperature", [0.0, 1.0])
+def test_sampling_with_inconsistent_offsets_and_parents(temperature):
+    m = d2sd()
+    rng = np.random.default_rng(8)
+    batch, total, max_nodes, V = 4, 120, 50, 1000
+    logits = torch.randn(total, V, device="cuda").to(torch.bfloat16)
+    uniform = torch.rand(total, device="cuda")
+    tbuf, tokens = guarded((total,), torch.int32, -7)
+    rbuf, reps = guarded((total,), torch.int32, -7)
+    m.sample_targets(garbage_i32(rng, batch + 1), total, max_nodes, garbage_i32(rng, total), garbage_i32(rng, total),
+                     logits, temperature, uniform=uniform if temperature else None, want_rep=True, out=tokens,
+                     rep_out=reps)
+    torch.cuda.synchronize()
+    assert guard_intact(tbuf, tokens.shape, -7) and guard_intact(rbuf, reps.shape, -7)
