@@ -558,20 +558,22 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
 // Fast copy of a full context tile. A four-row block lies in one page (tiles
 // start on page boundaries), so its source is a wave-uniform page base plus a
 // per-lane offset that depends only on the lane and the block's row within
-// the page, which is the same for every block of a wave.
-__device__ __forceinline__ void dma_ctx_tile(const Params& p, int key0, int c0, const int* s_pid, int wave_s,
-                                             uint32_t koff, uint32_t voff, const char* sK, const char* sV) {
+// the page, which is the same for every block of a wave. The copy takes the
+// staged page ids (page * hkv + h) of the wave's blocks, read beforehand by
+// ctx_tile_pages, so that the steady state can read them a step ahead.
+constexpr int kPagesPerTile = bf::KT / D2SD_PAGE_SIZE;
+__device__ __forceinline__ void ctx_tile_pages(const int* s_pid, int tile, int wave_s, int (&ph)[bf::WAVE_BLOCKS]) {
+#pragma unroll
+  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) ph[j] = s_pid[kPagesPerTile * tile + ((wave_s + bf::WAVES * j) >> 2)];
+}
+__device__ __forceinline__ void dma_ctx_pages(const Params& p, const int (&ph)[bf::WAVE_BLOCKS], int wave_s,
+                                              uint32_t koff, uint32_t voff, const char* sK, const char* sV) {
   const char* kc = static_cast<const char*>(p.k_cache);
   const char* vc = static_cast<const char*>(p.v_cache);
-  const int pg0 = (key0 - c0) >> 4;
-  uint32_t ph[bf::WAVE_BLOCKS];               // page * hkv + h of each block (read first: one LDS wait)
-#pragma unroll
-  for (int j = 0; j < bf::WAVE_BLOCKS; ++j)
-    ph[j] = (uint32_t)__builtin_amdgcn_readfirstlane(s_pid[pg0 + ((wave_s + bf::WAVES * j) >> 2)]);
 #pragma unroll
   for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
     const uint32_t blk = wave_s + bf::WAVES * j;
-    const size_t off = (size_t)ph[j] << 12;    // 16 rows x 256 B per (page, KV head)
+    const size_t off = (size_t)(uint32_t)__builtin_amdgcn_readfirstlane(ph[j]) << 12;  // 16 rows x 256 B
     dma16s(kc + off, koff, lds_addr(sK) + blk * 1024u);
     dma16s(vc + off, voff, lds_addr(sV) + blk * 1024u);
   }
@@ -790,9 +792,11 @@ void cascade_bf16_kernel(Params p) {
   const uint32_t voff = prow * bf::ROW_BYTES + (((lane & 15) ^ ((prow & 3) << 2)) << 4);
   auto copy_tile = [&](int j, const char* sK, const char* sV) {
     const TileSrc ts = src(j);
-    if (!ts.tree && ts.key_end - ts.key0 >= bf::KT)
-      dma_ctx_tile(p, ts.key0, c0, s_pid, wave_s, koff, voff, sK, sV);
-    else
+    if (!ts.tree && ts.key_end - ts.key0 >= bf::KT) {
+      int ph[bf::WAVE_BLOCKS];
+      ctx_tile_pages(s_pid, j, wave_s, ph);
+      dma_ctx_pages(p, ph, wave_s, koff, voff, sK, sV);
+    } else
       dma_tile(p, ts, h, node_base, s_pid, c0, dl, const_cast<char*>(sK), const_cast<char*>(sV));
   };
 
@@ -820,7 +824,30 @@ void cascade_bf16_kernel(Params p) {
     softmax_tile(s, m_run, l_run, o, pf, p.c2);
     pv_tile(cV, rl, pf, o);
   };
-  for (int jt = 0; jt < n_tiles; jt += 2) {
+  // Steady state: the tile consumed and the tile queued are both whole
+  // context tiles, so the step needs no masking, no choice of copy path, and
+  // reads the page ids of the tile it will queue next one step ahead (the
+  // staged page list does not change after the prologue).
+  const int n_full = c1 > c0 ? (c1 - c0) / bf::KT : 0;
+  int ph_next[bf::WAVE_BLOCKS];
+  if (n_full > 2) ctx_tile_pages(s_pid, 1, wave_s, ph_next);
+  auto fast_step = [&](int jt, const char* cK, const char* cV, const char* nK, const char* nV) {
+    sync_keep<0>();
+    dma_ctx_pages(p, ph_next, wave_s, koff, voff, nK, nV);    // tile jt + 1
+    if (jt + 2 < n_full) ctx_tile_pages(s_pid, jt + 2, wave_s, ph_next);
+    if (!active) return;
+    f32x16 s[bf::NKB];
+    qk_tile(cK, rl, q, s);
+    bf16x8 pf[2 * bf::NKB];
+    softmax_tile(s, m_run, l_run, o, pf, p.c2);
+    pv_tile(cV, rl, pf, o);
+  };
+  int jt = 0;
+  for (; jt + 2 < n_full; jt += 2) {   // both steps queue a whole context tile
+    fast_step(jt, sk0, sv0, sk1, sv1);
+    fast_step(jt + 1, sk1, sv1, sk0, sv0);
+  }
+  for (; jt < n_tiles; jt += 2) {      // the rest: partial and tree tiles (stage parity kept)
     step(jt, sk0, sv0, sk1, sv1);
     if (jt + 1 < n_tiles) step(jt + 1, sk1, sv1, sk0, sv0);
   }
