@@ -106,6 +106,21 @@ def test_poisoned_slack_is_never_read():
     check_full(Case(lay, poison_slack=True), "cascade", kv_split=64)
 
 
+@pytest.mark.parametrize("kv_split", [0, 64, 128, 192])
+def test_whole_tile_counts_around_the_steady_state(kv_split):
+    """Context lengths giving 0-5 whole 32-key tiles per split, with and
+    without a ragged tail, so that the steady-state loop (taken while the
+    tile consumed and the tile queued are both whole context tiles) hands
+    over to the general loop at every count and stage parity."""
+    ctx = [0, 1, 31, 32, 33, 63, 64, 65, 95, 96, 97, 127, 128, 129, 160, 161, 192, 200]
+    rng = np.random.default_rng(kv_split)
+    p_rows = [sorted(rng.choice(np.arange(1, 16), size=int(rng.integers(0, 4)), replace=False).tolist())
+              for _ in ctx]
+    lay = wl.custom_layout(16, p_rows, ctx, hq=8, hkv=2, dtype="bf16", seed=16)
+    check_full(Case(lay, poison_slack=True), "cascade", kv_split=kv_split)
+    check_full(Case(lay), "prefix", kv_split=kv_split)
+
+
 def test_large_block_trees():
     # B = 64: up to 2080 nodes, masks of 65 words, many tree tiles
     lay = wl.custom_layout(64, [list(range(1, 64)), [10, 30]], [100, 0], hq=4, hkv=2, dtype="bf16", seed=15)
