@@ -173,7 +173,7 @@ def record_traffic(d: str):
 
 def _workload_names() -> dict:
     from paper_2606_04446_amd import workload as wl
-    return {k: v.name for k, v in wl.CONFIGS.items()}
+    return {k: v.name for k, v in wl.WORKLOADS.items()}
 
 
 def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float, parents=None):

@@ -56,7 +56,7 @@ class Spec:
 # [1, B-1]. p_rule "beta_lowest": per-position confidence c_j ~ Beta(5, 2),
 # j = 1..B-1, and the K positions with the lowest confidence (ties to the
 # smaller j) become the re-anchor positions.
-CONFIGS = {
+WORKLOADS = {
     1: Spec("ctx512-b1-fp32", "f32", 1, (512, 512), 32, 8, K=2, p_rule="uniform",
             permute_pages=False),
     2: Spec("ctx4096-b1-bf16", "bf16", 1, (4096, 4096), 32, 8, K=4),
@@ -128,7 +128,7 @@ def pages_for(ctx_len: Sequence[int], page_size: int, permute: bool,
 def draw_layout(cfg, seed: Optional[int] = None) -> Layout:
     """Layout of a numbered workload (seed defaults to the workload number) or of a Spec."""
     if isinstance(cfg, int):
-        spec = CONFIGS[cfg]
+        spec = WORKLOADS[cfg]
         seed = cfg if seed is None else seed
     else:
         spec = cfg

@@ -21,7 +21,7 @@ def trees_of(layout):
 def test_layout_recipe(cfg):
     a, b = wl.draw_layout(cfg), wl.draw_layout(cfg)
     assert np.array_equal(a.p, b.p) and np.array_equal(a.page_table, b.page_table)
-    spec = wl.CONFIGS[cfg]
+    spec = wl.WORKLOADS[cfg]
     assert a.batch == spec.batch and (a.K == spec.K).all()
     lo, hi = spec.ctx
     assert ((a.ctx_len >= lo) & (a.ctx_len <= hi)).all()
