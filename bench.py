@@ -1,19 +1,22 @@
 """Benchmark of one verify step on one MI355X: tree build -> cascade verify
 attention -> accept path, on a seeded synthetic batch resident in HBM.
 
-    python bench.py [--steps K] [--warmup W] [--config 4] [--kv-split S]
+    python bench.py [--steps K] [--warmup W] [--config 5] [--kv-split S]
                     [--cpu-seconds 15] [--no-cpu-baseline] [--noncascade]
                     [--tree canonical|third_level|resample] [--graph]
                     [--temperature 1.0] [--sample-vocab 32000]
+    python bench.py --profile-stage tree|prefix|cascade   (attention calls of one stage only, for counters)
     python bench.py --copy-probe       (HBM counter calibration copy)
 
-Prints one JSON line. value = verified tree tokens per second of the whole
-step (tree nodes verified / step time, K steps back to back). The roofline
-object describes the cascade attention kernel (the step's dominant kernel),
-timed with HIP events recorded by the library on its launch stream over the
-timed steps. `timing` adds per-step median / p10 / p90 of the step and of the
-attention kernel, warm (back to back) and cold (each step after a 512 MiB
-write that evicts every cache level).
+Prints one JSON line. Default workload: 64 requests x 32768-token contexts,
+64 query / 8 KV heads, bf16 (the largest one-GPU workload). The K timed steps
+each follow a 512 MiB cache-evicting write (outside the step's own event
+pair), so every input comes from HBM; ms_per_step is their median and value =
+verified tree tokens per second of the whole step (tree nodes / ms_per_step).
+The roofline object describes the cascade attention operation (its main
+kernel plus the split merge when the context is split), timed with HIP events
+that the library records on its launch stream over the timed steps. `timing`
+adds the same steps back to back (warm) beside the cold ones.
 """
 
 from __future__ import annotations
@@ -50,11 +53,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--kv-split", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--noncascade", action="store_true", help="also time the non-cascade baseline kernel")
+    ap.add_argument("--noncascade", action="store_true",
+                    help="also time the non-cascade baseline kernel (always on for workload 5)")
+    ap.add_argument("--profile-stage", choices=["cascade", "prefix", "tree"],
+                    help="only run W + K attention calls of this stage on the workload (no step, no oracle), "
+                         "e.g. the tree-suffix tiles alone for MFMA counters; prints a short JSON line")
     ap.add_argument("--tree", choices=["canonical", "third_level", "resample"], default="canonical",
                     help="tree shape: the canonical chain-plus-branches tree (default), the third-level cascade "
                          "(a sub-branch inside every branch) or K+1 resampled chains, the latter two built from "
@@ -149,6 +156,10 @@ def record_traffic(d: str):
     kern = "cascade_bf16_kernel" if bench["dtype"] == "bf16" else "cascade_attention_kernel"
     fetch = _counter_per_dispatch(os.path.join(d, "fetch"), kern, "FETCH_SIZE")
     write = _counter_per_dispatch(os.path.join(d, "write"), kern, "WRITE_SIZE")
+    if bench.get("roofline", {}).get("splits", 1) > 1:
+        # the split merge reads the partial states back: part of the same operation
+        fetch += _counter_per_dispatch(os.path.join(d, "fetch"), "split_merge_kernel", "FETCH_SIZE")
+        write += _counter_per_dispatch(os.path.join(d, "write"), "split_merge_kernel", "WRITE_SIZE")
     copy_kib = (1 << 30) / 1024.0
     f_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_fetch"), "copyBuffer", "FETCH_SIZE")
     w_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_write"), "copyBuffer", "WRITE_SIZE")
@@ -174,6 +185,57 @@ def record_traffic(d: str):
 def _workload_names() -> dict:
     from paper_2606_04446_amd import workload as wl
     return {k: v.name for k, v in wl.WORKLOADS.items()}
+
+
+def bench_parent_array(B: int, p_row, q_row=None, chains: int = 0) -> np.ndarray:
+    """Parent array (local indices, node 0 the anchor) of one request's tree:
+    the input of the parent-array tree builder for the --tree shapes (the
+    third-level cascade of sec. 4.3 and resampled chains):
+      chains > 0  `chains` independent chains of B-1 drafts under the anchor;
+      otherwise   the first-draft chain, one branch per re-anchor position p
+                  (ascending) hanging under the chain node at p - 1, and, when
+                  q_row is given, per branch a sub-branch hanging under the
+                  branch node at q - 1 (q > p; 0 = none), after all branches."""
+    par = [-1]
+    if chains > 0:
+        for _ in range(chains):
+            prev = 0
+            for _ in range(B - 1):
+                par.append(prev)
+                prev = len(par) - 1
+        return np.asarray(par, np.int32)
+    for j in range(1, B):
+        par.append(j - 1)
+    order = sorted(range(len(p_row)), key=lambda k: p_row[k])
+    at = {}                                     # (branch, position) -> node
+    for k in order:
+        pk = int(p_row[k])
+        prev = pk - 1
+        for pos in range(pk, B):
+            par.append(prev)
+            prev = len(par) - 1
+            at[(k, pos)] = prev
+    if q_row is not None:
+        for k in order:
+            qk = int(q_row[k])
+            if qk <= 0:
+                continue
+            prev = at[(k, qk - 1)] if qk - 1 >= int(p_row[k]) else qk - 1
+            for _ in range(qk, B):
+                par.append(prev)
+                prev = len(par) - 1
+    return np.asarray(par, np.int32)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float, parents=None):
@@ -216,13 +278,15 @@ def cpu_baseline(x, layout, node_indptr, parent_host, budget_s: float, parents=N
                 one_thread = (e - s) / (time.perf_counter() - t1)
         if t_total >= budget_s:
             break
-    blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
-    cores = max(blas) if blas else 1
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    cores = max([i.get("num_threads", 1) for i in blas] or [1])
+    blas_name = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}" for i in blas})) or "unknown"
     res = {
         "value": done_nodes / t_total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
         "sample": f"{done_req} of {layout.batch} requests (tree build + float64 attention of every node "
                   f"and query head over the full context and its ancestors), {t_total:.1f} s, "
                   f"{len(os.sched_getaffinity(0))} host cores visible",
+        "cpu_model": cpu_model(), "blas": blas_name,
     }
     if layout.batch == 1:
         res["value_1_thread"] = one_thread
@@ -258,8 +322,8 @@ def main():
         node_indptr, W = d2sd.tree_plan(B, layout.K, layout.p)
     else:
         q_sub = wl.draw_sub_branch_positions(layout)
-        parents = [wl.parent_array(B, layout.p[b, :layout.K[b]], q_sub[b, :layout.K[b]])
-                   if args.tree == "third_level" else wl.parent_array(B, [], chains=int(layout.K[b]) + 1)
+        parents = [bench_parent_array(B, layout.p[b, :layout.K[b]], q_sub[b, :layout.K[b]])
+                   if args.tree == "third_level" else bench_parent_array(B, [], chains=int(layout.K[b]) + 1)
                    for b in range(layout.batch)]
         node_indptr = np.concatenate([[0], np.cumsum([len(pa) for pa in parents])]).astype(np.int32)
         W = (int(np.diff(node_indptr).max()) + 31) // 32
@@ -285,50 +349,67 @@ def main():
     lse = torch.empty(x["q"].shape[:2], dtype=torch.float32, device=dev)
     a = d2sd.attn_args(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"], d_ip,
                        tree["anc_mask"], out, lse, total_nodes=total, max_nodes=max_nodes, max_ctx_len=max_ctx,
-                       kv_split=args.kv_split)
+                       kv_split=args.kv_split, node_indptr_host=node_indptr)
     ws_bytes = d2sd.cascade_workspace_size(a)
     kv_split = d2sd.cascade_kv_split(a)
+    n_splits = -(-max_ctx // kv_split) if max_ctx > 0 else 1
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     acc = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax)
 
-    def step():
-        build(out=tree)
+    def attention(stage=d2sd.STAGE_CASCADE, o=out, l=lse):
         d2sd.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"],
                                       d_ip, tree["anc_mask"], total_nodes=total, max_nodes=max_nodes,
-                                      max_ctx_len=max_ctx, kv_split=args.kv_split, out=out, lse=lse,
-                                      workspace=ws)
+                                      max_ctx_len=max_ctx, stage=stage, kv_split=args.kv_split, out=o, lse=l,
+                                      workspace=ws, node_indptr_host=node_indptr)
+
+    if args.profile_stage:
+        # Attention calls of one stage only (e.g. the tree-suffix tiles alone),
+        # for counter runs that must see nothing else.
+        stage = {"cascade": d2sd.STAGE_CASCADE, "prefix": d2sd.STAGE_PREFIX, "tree": d2sd.STAGE_TREE}[args.profile_stage]
+        for _ in range(args.warmup):
+            attention(stage)
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_collect_parts()
+        d2sd.kernel_timing_enable(True)
+        for _ in range(args.steps):
+            attention(stage)
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_enable(False)
+        kern, merge = d2sd.kernel_timing_collect_parts()
+        depth = tree["depth"].cpu().numpy().astype(np.int64)
+        tree_keys = float((depth + 1).sum())                       # visible tree keys per (node, query head)
+        flops = 4.0 * spec.hq * spec.head_dim * (tree_keys if stage == d2sd.STAGE_TREE else
+                                                 float(np.repeat(layout.ctx_len.astype(np.int64),
+                                                                 np.diff(node_indptr)).sum())
+                                                 + (tree_keys if stage == d2sd.STAGE_CASCADE else 0.0))
+        k_ms = float(np.mean(kern))
+        print(json.dumps({"profile_stage": args.profile_stage, "workload": spec.name, "calls": len(kern),
+                          "kernel_ms": round(k_ms, 4), "merge_ms": round(float(np.mean(merge)), 4),
+                          "algorithmic_flop_per_call": flops, "tflops": round(flops / (k_ms / 1e3) / 1e12, 3),
+                          "kv_split": kv_split}), flush=True)
+        return
+
+    def step():
+        build(out=tree)
+        attention()
         d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax,
                          out=acc)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    d2sd.kernel_timing_collect()
-    d2sd.kernel_timing_enable(True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
-        step()
-    ev1.record()
-    torch.cuda.synchronize()
-    d2sd.kernel_timing_enable(False)
-    step_ms_eager = ev0.elapsed_time(ev1) / args.steps
-    launches, kern_ms_total = d2sd.kernel_timing_collect()
-    kern_ms = kern_ms_total / max(launches, 1)
-
-    # Per-step distributions, outside the timed bracket above: the steps run
-    # back to back as there, with an event pair around each step and the
-    # library's events around each attention launch. "warm": nothing between
-    # steps; "cold": a 512 MiB write before every step evicts the L2 caches
-    # and the 256 MB Infinity Cache, so every input is read from HBM.
     flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
 
-    def per_step(reps, flush):
+    def timed_steps(reps, flush):
+        """reps steps, each bracketed by its own event pair; with flush, a
+        512 MiB write before each step (outside its pair) evicts the L2
+        caches and the 256 MB Infinity Cache, so every input comes from HBM.
+        Returns the per-step times and the library's per-call attention
+        kernel and split-merge times (ms)."""
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-        torch.cuda.synchronize()
-        d2sd.kernel_timing_collect_each()
+        d2sd.kernel_timing_collect_parts()
         d2sd.kernel_timing_enable(True)
+        torch.cuda.synchronize()
         for i, (e_a, e_b) in enumerate(evs):
             if flush:
                 flush_buf.fill_(i & 0xff)
@@ -337,38 +418,56 @@ def main():
             e_b.record()
         torch.cuda.synchronize()
         d2sd.kernel_timing_enable(False)
-        attn_t = d2sd.kernel_timing_collect_each()
-        return {"step_ms": percentiles([e_a.elapsed_time(e_b) for e_a, e_b in evs]),
-                "attn_ms": percentiles(attn_t)}
+        kern, merge = d2sd.kernel_timing_collect_parts()
+        return [e_a.elapsed_time(e_b) for e_a, e_b in evs], kern, merge
 
-    timing = {"reps": args.steps, "warm": per_step(args.steps, False), "cold": per_step(args.steps, True),
-              "flush_bytes": FLUSH_BYTES}
+    # The timed region: K cold steps (the headline), bracketed by synchronisations.
+    step_cold, kern_cold, merge_cold = timed_steps(args.steps, True)
+    # The same steps back to back (warm), and K back-to-back steps between one event pair.
+    step_warm, kern_warm, merge_warm = timed_steps(args.steps, False)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    step_ms_backtoback = ev0.elapsed_time(ev1) / args.steps
     del flush_buf
 
+    op_cold = [k + m for k, m in zip(kern_cold, merge_cold)]
+    timing = {"reps": args.steps, "flush_bytes": FLUSH_BYTES,
+              "cold": {"step_ms": percentiles(step_cold), "attn_ms": percentiles(op_cold),
+                       "attn_kernel_ms": percentiles(kern_cold), "merge_ms": percentiles(merge_cold)},
+              "warm": {"step_ms": percentiles(step_warm),
+                       "attn_ms": percentiles([k + m for k, m in zip(kern_warm, merge_warm)]),
+                       "attn_kernel_ms": percentiles(kern_warm), "merge_ms": percentiles(merge_warm)},
+              "backtoback_step_ms": round(step_ms_backtoback, 4)}
+    step_ms_cold = float(np.median(step_cold))
+    op_ms = float(np.mean(op_cold))                 # attention operation: kernel + split merge
+    kern_ms = float(np.mean(kern_cold))
+    merge_ms = float(np.mean(merge_cold))
+
     # The prefix stage alone (context keys only, no tree tiles): the time
-    # that the prefix K/V bandwidth is quoted against, beside the whole
-    # attention call.
+    # that the prefix K/V bandwidth is also quoted against.
     out_p, lse_p = torch.empty_like(out), torch.empty_like(lse)
-    prefix_call = lambda: d2sd.cascade_verify_attention(
-        x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"], d_ip, tree["anc_mask"],
-        total_nodes=total, max_nodes=max_nodes, max_ctx_len=max_ctx, stage=d2sd.STAGE_PREFIX,
-        kv_split=args.kv_split, out=out_p, lse=lse_p, workspace=ws)
     for _ in range(args.warmup):
-        prefix_call()
+        attention(d2sd.STAGE_PREFIX, out_p, lse_p)
     torch.cuda.synchronize()
-    d2sd.kernel_timing_collect_each()
+    d2sd.kernel_timing_collect_parts()
     d2sd.kernel_timing_enable(True)
     for _ in range(args.steps):
-        prefix_call()
+        attention(d2sd.STAGE_PREFIX, out_p, lse_p)
     torch.cuda.synchronize()
     d2sd.kernel_timing_enable(False)
-    prefix_ms = float(np.mean(d2sd.kernel_timing_collect_each()))
+    pk, pm = d2sd.kernel_timing_collect_parts()
+    prefix_ms = float(np.mean(pk)) + float(np.mean(pm))
     del out_p, lse_p
 
-    # The same step captured once in a HIP graph and replayed: the four
-    # launches of a step then cost one graph launch (the step allocates
-    # nothing and issues no memset, so it can be captured as it is).
-    step_ms = step_ms_eager
+    # The same step captured once in a HIP graph and replayed (the step
+    # allocates nothing and issues no memset, so it can be captured as it is).
+    step_ms = step_ms_cold
+    graph_ms = None
     if args.graph:
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
@@ -387,9 +486,9 @@ def main():
             graph.replay()
         ev1.record()
         torch.cuda.synchronize()
-        step_ms = ev0.elapsed_time(ev1) / args.steps
+        graph_ms = ev0.elapsed_time(ev1) / args.steps
 
-    # algorithmic work of one launch of the cascade kernel
+    # algorithmic work of one attention operation
     esz = 2 if spec.dtype == "bf16" else 4
     D, Hq, Hkv = spec.head_dim, spec.hq, spec.hkv
     ctx = layout.ctx_len.astype(np.int64)
@@ -398,18 +497,20 @@ def main():
     n_per_req = np.diff(node_indptr).astype(np.int64)
     visible = np.repeat(ctx, n_per_req) + depth + 1          # keys each node attends to
     flops = 4.0 * Hq * D * float(visible.sum())
-    t_s = kern_ms / 1e3
+    t_s = op_ms / 1e3
     gbps = prefix_bytes / t_s / 1e9
     tflops = flops / t_s / 1e12
     t_hbm = prefix_bytes / (HBM_PEAK_GBPS * 1e9)
     t_mfma = flops / (MFMA_PEAK_TFLOPS[spec.dtype] * 1e12)
     traffic = measured_traffic(args.config, args.kv_split, kv_split) if args.tree == "canonical" else None
+    parts = {"kernel_ms": round(kern_ms, 4), "merge_ms": round(merge_ms, 4), "splits": n_splits}
     if t_mfma > t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_PEAK_TFLOPS[spec.dtype],
-                "unit": "TFLOP/s", "frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4), "traffic": traffic}
+                "unit": "TFLOP/s", "frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4), "traffic": traffic,
+                **parts}
     else:
         roof = {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": traffic}
+                "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": traffic, **parts}
 
     res = {
         "metric": METRIC,
@@ -419,8 +520,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(step_ms, 4),
-        "ms_per_step_eager": round(step_ms_eager, 4),
+        "ms_per_step_timing": "median of the K timed steps, each after a 512 MiB cache-evicting write",
         "graph": bool(args.graph),
+        "graph_replay_ms_per_step": round(graph_ms, 4) if graph_ms is not None else None,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -431,20 +533,24 @@ def main():
                    "head_dim": D, "block": B, "branches": spec.K, "tree_nodes": total,
                    "page_size": spec.page_size, "kv_split": kv_split, "tree": args.tree},
         "roofline": roof,
+        "roofline_note": ("mfma-bound: the workload's algorithmic flops at the bf16 dense peak take longer "
+                          "than its prefix K/V bytes at the HBM peak" if roof["bound"] == "mfma" else
+                          "hbm-bound: the prefix K/V bytes at the HBM peak take longer than the flops at the "
+                          "MFMA peak"),
         "prefix_kv_gbps": round(gbps, 1),
         "prefix_kv_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
-        "prefix_stage": {"kernel_ms": round(prefix_ms, 4),
+        "prefix_stage": {"ms": round(prefix_ms, 4),
                          "prefix_kv_gbps": round(prefix_bytes / (prefix_ms / 1e3) / 1e9, 1),
                          "prefix_kv_hbm_frac": round(prefix_bytes / (prefix_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)},
         "attn_tflops": round(tflops, 2),
         "attn_mfma_frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4),
-        "attn_kernel_ms": round(kern_ms, 4),
+        "attn_ms": round(op_ms, 4),
         "attn_tokens_per_s": round(total / t_s, 1),
         "kernel_sha": kernel_sha(),
         "requested_kv_split": args.kv_split,
         "timing": timing,
     }
-    if args.noncascade:
+    if args.noncascade or args.config == 5:
         out2 = torch.empty_like(out)
         lse2 = torch.empty_like(lse)
         reps = 3
@@ -461,7 +567,7 @@ def main():
         d2sd.kernel_timing_enable(False)
         n, ms = d2sd.kernel_timing_collect()
         nc_ms = ms / max(n, 1)
-        res["noncascade"] = {"kernel_ms": round(nc_ms, 3), "speedup_of_cascade": round(nc_ms / kern_ms, 2),
+        res["noncascade"] = {"kernel_ms": round(nc_ms, 3), "speedup_of_cascade": round(nc_ms / op_ms, 2),
                              "requested_prefix_bytes": int((np.repeat(ctx, n_per_req)).sum()) * Hkv * D * 2 * esz,
                              "max_abs_diff_vs_cascade": float((out2.float() - out.float()).abs().max())}
     # Device re-anchor selection (Eq. 4-5) and node offsets for the same batch,

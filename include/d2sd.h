@@ -7,10 +7,11 @@
  *   d2sd_tree_plan        host    validate (B, p_k), node counts, mask width
  *   d2sd_tree_build       device  canonical tree arrays + ancestor-or-self masks
  *   d2sd_cascade_verify_attention
- *                         device  shared-prefix (context) attention, read once per
- *                                 KV head for every tree node and GQA head, plus
- *                                 tree-suffix attention under the ancestor mask,
- *                                 states merged by log-sum-exp
+ *                         device  shared-prefix (context) attention, each context
+ *                                 slab read once per (split, 128-row group) and
+ *                                 shared by the tree nodes and GQA heads of the
+ *                                 group, plus tree-suffix attention under the
+ *                                 ancestor mask, states merged by log-sum-exp
  *   d2sd_merge_state      device  the log-sum-exp merge of two attention states
  *   d2sd_accept_path      device  greedy longest-accepted-path selection + bonus
  *   d2sd_sample_targets   device  target token per node from logits: draw at
@@ -226,6 +227,8 @@ d2sd_status d2sd_tree_indptr(int batch, int B, int Kmax, const int* K, const int
  *   anc_mask [total_nodes, mask_words] uint32 (from d2sd_tree_build)
  *   out      [total_nodes, num_qo_heads, head_dim]
  *   lse      [total_nodes, num_qo_heads] fp32, natural log; nullable
+ * q, k_cache, v_cache, k_tree, v_tree and out must be 16-byte aligned (the
+ * kernels move them in 16-byte chunks); INVALID_ARG otherwise.
  * STAGE_PREFIX writes the normalised context-only state (rows of a request
  * with ctx_len 0 get out = 0, lse = -inf); STAGE_TREE the tree-only state.
  */
@@ -256,6 +259,10 @@ typedef struct d2sd_attn_args {
   const uint32_t* anc_mask;
   void* out;
   float* lse;
+  const int* node_indptr_host; /* nullable: host copy of node_indptr; when given
+                                  (and valid: starts at 0, ends at total_nodes,
+                                  every request within max_nodes) the automatic
+                                  split counts the work items exactly */
 } d2sd_attn_args;
 
 /*
@@ -272,11 +279,14 @@ d2sd_status d2sd_cascade_workspace_size(const d2sd_attn_args* args, size_t* byte
 d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split);
 
 /*
- * Device. Verify attention (see d2sd_attn_args). Every context page slab of a
- * (request, KV head) is streamed from HBM once per split and reused by all
- * G query heads of all N_b tree nodes. ws: device workspace of ws_bytes >=
- * d2sd_cascade_workspace_size(args) (may be NULL when that size is 0).
- * Concurrent calls must not share a workspace.
+ * Device. Verify attention (see d2sd_attn_args). The M = N_b * G query rows
+ * of a (request, KV head) are cut into row groups of 128 (bf16); every
+ * context page slab is streamed once per (context split, row group) and
+ * reused by all 128 rows of the group, i.e. by all G query heads of the
+ * group's tree nodes. The row groups of one split run as neighbouring
+ * workgroups on one XCD, so that later readers of a slab mostly hit its L2.
+ * ws: device workspace of ws_bytes >= d2sd_cascade_workspace_size(args) (may
+ * be NULL when that size is 0). Concurrent calls must not share a workspace.
  */
 d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, size_t ws_bytes,
                                           hipStream_t stream);
@@ -415,21 +425,30 @@ d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head
 
 /*
  * Host. When enabled (nonzero), d2sd_cascade_verify_attention and
- * d2sd_noncascade_verify_attention record a HIP event pair on their stream
- * around their main (context-streaming) kernel. d2sd_kernel_timing_collect
- * waits for the recorded events, returns the launch count and the summed
- * duration in milliseconds, and clears the record. Thread-safe.
+ * d2sd_noncascade_verify_attention record HIP events on their stream before
+ * their main (context-streaming) kernel, after it, and after the split merge
+ * that follows it when the context is split. d2sd_kernel_timing_collect
+ * waits for the recorded events, returns the call count and the summed
+ * duration of the whole attention operation (main kernel + split merge) in
+ * milliseconds, and clears the record. Thread-safe.
  */
 d2sd_status d2sd_kernel_timing_enable(int enable);
 d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms);
 
 /*
  * Host. As d2sd_kernel_timing_collect, but writes the duration of each
- * recorded launch (milliseconds, launch order) to ms_each[0 .. min(n,
- * capacity)) (host memory, caller-owned) and the launch count n to
- * *launches; durations past capacity are dropped. Clears the record.
+ * recorded call (main kernel + split merge, milliseconds, call order) to
+ * ms_each[0 .. min(n, capacity)) (host memory, caller-owned) and the call
+ * count n to *launches; durations past capacity are dropped. Clears the record.
  */
 d2sd_status d2sd_kernel_timing_collect_each(int capacity, float* ms_each, int* launches);
+
+/*
+ * Host. As d2sd_kernel_timing_collect_each, with the two parts of each call
+ * apart: kernel_ms[i] the main kernel, merge_ms[i] the split merge (0 when
+ * the call had none). Clears the record.
+ */
+d2sd_status d2sd_kernel_timing_collect_parts(int capacity, float* kernel_ms, float* merge_ms, int* launches);
 
 #ifdef __cplusplus
 }

@@ -36,7 +36,10 @@ d2sd_status hip_status(hipError_t e, const char* what) {
 // ---- kernel timing (HIP events around the context-streaming kernel) ----
 std::mutex g_timing_mu;
 bool g_timing_on = false;
-std::vector<std::pair<hipEvent_t, hipEvent_t>> g_timing_pending;
+struct TimedLaunch {
+  hipEvent_t e0, e1, e2;  // before the main kernel, after it, after the split merge
+};
+std::vector<TimedLaunch> g_timing_pending;
 std::vector<hipEvent_t> g_event_pool;
 
 hipEvent_t take_event() {
@@ -50,43 +53,48 @@ hipEvent_t take_event() {
   return e;
 }
 
-// Reserve an event pair when timing is on (both null otherwise).
-void timing_begin(hipEvent_t* e0, hipEvent_t* e1) {
-  *e0 = *e1 = nullptr;
+// Reserve three events when timing is on (all null otherwise).
+void timing_begin(hipEvent_t (&ev)[3]) {
+  ev[0] = ev[1] = ev[2] = nullptr;
   std::lock_guard<std::mutex> lk(g_timing_mu);
   if (!g_timing_on) return;
-  *e0 = take_event();
-  *e1 = take_event();
-  if (!*e0 || !*e1) {
-    if (*e0) g_event_pool.push_back(*e0);
-    if (*e1) g_event_pool.push_back(*e1);
-    *e0 = *e1 = nullptr;
+  for (auto& e : ev) e = take_event();
+  if (!ev[0] || !ev[1] || !ev[2]) {
+    for (auto& e : ev) {
+      if (e) g_event_pool.push_back(e);
+      e = nullptr;
+    }
     return;
   }
-  g_timing_pending.emplace_back(*e0, *e1);
+  g_timing_pending.push_back({ev[0], ev[1], ev[2]});
 }
 
-// Wait for every recorded event pair, return each duration (ms) in launch
-// order, recycle the events and clear the record.
-hipError_t collect_timings(std::vector<float>* each) {
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> pend;
+// Wait for every recorded launch and return, in launch order, the main
+// kernel's duration and the split merge's (ms; 0 when the call had no
+// merge); recycle the events and clear the record.
+hipError_t collect_timings(std::vector<float>* kernel, std::vector<float>* merge) {
+  std::vector<TimedLaunch> pend;
   {
     std::lock_guard<std::mutex> lk(g_timing_mu);
     pend.swap(g_timing_pending);
   }
   hipError_t err = hipSuccess;
-  each->reserve(pend.size());
-  for (auto& pr : pend) {
-    float ms = 0.0f;
-    hipError_t e = hipEventSynchronize(pr.second);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
+  kernel->reserve(pend.size());
+  merge->reserve(pend.size());
+  for (auto& t : pend) {
+    float k_ms = 0.0f, m_ms = 0.0f;
+    hipError_t e = hipEventSynchronize(t.e2);
+    if (e == hipSuccess) e = hipEventElapsedTime(&k_ms, t.e0, t.e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&m_ms, t.e1, t.e2);
     if (e != hipSuccess && err == hipSuccess) err = e;
-    each->push_back(ms);
+    kernel->push_back(k_ms);
+    merge->push_back(m_ms);
   }
   std::lock_guard<std::mutex> lk(g_timing_mu);
-  for (auto& pr : pend) {
-    g_event_pool.push_back(pr.first);
-    g_event_pool.push_back(pr.second);
+  for (auto& t : pend) {
+    g_event_pool.push_back(t.e0);
+    g_event_pool.push_back(t.e1);
+    g_event_pool.push_back(t.e2);
   }
   return err;
 }
@@ -144,34 +152,85 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
   if (a->stage != D2SD_STAGE_PREFIX && a->mask_words < (a->max_nodes + 31) / 32)
     return fail(D2SD_ERR_INVALID_ARG, "mask_words %d too small for max_nodes %d", a->mask_words,
                 a->max_nodes);
+  if (a->node_indptr_host) {
+    const int* ip = a->node_indptr_host;
+    if (ip[0] != 0 || ip[a->batch] != a->total_nodes)
+      return fail(D2SD_ERR_INVALID_ARG, "node_indptr_host must start at 0 and end at total_nodes %d (got %d, %d)",
+                  a->total_nodes, ip[0], ip[a->batch]);
+    for (int b = 0; b < a->batch; ++b)
+      if (ip[b + 1] < ip[b] || ip[b + 1] - ip[b] > a->max_nodes)
+        return fail(D2SD_ERR_INVALID_ARG, "node_indptr_host: request %d has %d nodes, outside [0, max_nodes %d]",
+                    b, ip[b + 1] - ip[b], a->max_nodes);
+  }
   if (!need_ws_fields) return D2SD_OK;
   if (!a->q || !a->k_cache || !a->v_cache || !a->page_table || !a->ctx_len || !a->k_tree ||
       !a->v_tree || !a->node_indptr || !a->out)
     return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
   if (a->stage != D2SD_STAGE_PREFIX && !a->anc_mask)
     return fail(D2SD_ERR_INVALID_ARG, "anc_mask is NULL");
+  // the kernels move Q, K/V and the output in 16-byte chunks
+  const void* const chunked[] = {a->q, a->k_cache, a->v_cache, a->k_tree, a->v_tree, a->out};
+  const char* const names[] = {"q", "k_cache", "v_cache", "k_tree", "v_tree", "out"};
+  for (int i = 0; i < 6; ++i)
+    if (reinterpret_cast<uintptr_t>(chunked[i]) % 16 != 0)
+      return fail(D2SD_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
   return D2SD_OK;
 }
 
-// Context tokens per split. Automatic choice: enough (request, KV head, row
-// group, split) work items for about two rounds of resident workgroups (three
-// per CU for the 4-wave bf16 kernel, one otherwise), but no split shorter
-// than the dtype's minimum (the partial state of a split costs as many bytes
-// as ~M/2 keys of K/V, M = rows sharing it; fp32 splits are compute-bound and
-// can be shorter).
+// Row groups (work items) of one context split over the batch: exact when the
+// host copy of the node offsets is given, else from the mean tree size.
+long long groups_per_split(const d2sd_attn_args* a, int G) {
+  const int rows_per_group = d2sd::group_rows(a->dtype);
+  long long groups = 0;
+  if (a->node_indptr_host) {
+    for (int b = 0; b < a->batch; ++b) {
+      const long long rows = (long long)(a->node_indptr_host[b + 1] - a->node_indptr_host[b]) * G;
+      groups += (rows + rows_per_group - 1) / rows_per_group;
+    }
+  } else {
+    const double avg_rows = (double)a->total_nodes / a->batch * G;
+    groups = (long long)a->batch * max(1, (int)ceil(avg_rows / rows_per_group));
+  }
+  return max(1ll, groups * a->num_kv_heads);
+}
+
+// Context tokens per split (automatic choice). R = resident workgroups (three
+// per CU for the 4-wave bf16 kernel, one otherwise) and g = row groups per
+// split. When one split already gives at least R work items, work items of
+// equal length run in ceil(g s / R) rounds of resident workgroups, each 1/s
+// of a context long, so the kernel takes time in proportion to
+// ceil(g s / R) / s: the split count s minimising it is taken, a larger s
+// only for a gain of at least 3% (every split adds a partial state that the
+// merge reads back). Smaller grids take about two rounds of work items. No
+// split is shorter than the dtype's minimum (the partial state of a split
+// costs as many bytes as ~M/2 keys of K/V, M = rows sharing it; fp32 splits
+// are compute-bound and can be shorter) or longer than the staged page list
+// allows.
 int choose_split(const d2sd_attn_args* a, int G) {
   if (a->kv_split > 0) return a->kv_split;
   const int ctx = a->max_ctx_len;
   const int min_split = a->dtype == D2SD_F32 ? kMinSplitF32 : kMinSplit;
   if (ctx <= min_split) return ((max(ctx, 1) + 63) / 64) * 64;
-  const double avg_nodes = (double)a->total_nodes / a->batch;
-  const int avg_tiles = (int)ceil(avg_nodes * G / d2sd::kRowsPerTile);
-  const int tiles_per_group = d2sd::group_rows(a->dtype) / d2sd::kRowsPerTile;
-  const int avg_groups = max(1, (avg_tiles + tiles_per_group - 1) / tiles_per_group);
-  const long long base = (long long)a->batch * a->num_kv_heads * avg_groups;
-  const int resident = kNumCUs * (a->dtype == D2SD_BF16 ? 3 : 1);
-  int splits = (int)((2ll * resident + base - 1) / base);
-  splits = max(max(1, (ctx + kMaxSplit - 1) / kMaxSplit), min(splits, ctx / min_split));
+  const long long base = groups_per_split(a, G);
+  const long long resident = (long long)kNumCUs * (a->dtype == D2SD_BF16 ? 3 : 1);
+  const int s_lo = max(1, (ctx + kMaxSplit - 1) / kMaxSplit);
+  const int s_hi = max(s_lo, ctx / min_split);
+  int splits;
+  if (base * s_lo >= resident) {
+    auto rounds_per_split = [&](int s) { return (double)((base * s + resident - 1) / resident) / s; };
+    splits = s_lo;
+    double best = rounds_per_split(s_lo);
+    for (int s = s_lo + 1; s <= min(s_hi, 4 * s_lo); ++s) {
+      const double t = rounds_per_split(s);
+      if (t < 0.97 * best) {
+        best = t;
+        splits = s;
+      }
+    }
+  } else {
+    splits = (int)((2 * resident + base - 1) / base);
+    splits = max(s_lo, min(splits, s_hi));
+  }
   const int per = (ctx + splits - 1) / splits;
   return ((per + 63) / 64) * 64;
 }
@@ -324,6 +383,11 @@ d2sd_status d2sd_commit_accepted_kv(int batch, int B, int num_kv_heads, int head
   if (!node_indptr || !path_nodes || !accept_len || !k_tree || !v_tree || !page_table || !ctx_len || !k_cache ||
       !v_cache)
     return fail(D2SD_ERR_INVALID_ARG, "a required device pointer is NULL");
+  const void* const chunked[] = {k_tree, v_tree, k_cache, v_cache};
+  const char* const names[] = {"k_tree", "v_tree", "k_cache", "v_cache"};
+  for (int i = 0; i < 4; ++i)  // rows move in 16-byte chunks
+    if (reinterpret_cast<uintptr_t>(chunked[i]) % 16 != 0)
+      return fail(D2SD_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
   const int row_bytes = head_dim * (dtype == D2SD_BF16 ? 2 : 4);
   if ((long long)B * num_kv_heads * (row_bytes / 16) > 0x7fffffffll)
     return fail(D2SD_ERR_UNSUPPORTED, "B x num_kv_heads x %d chunks exceeds 2^31 - 1", row_bytes / 16);
@@ -363,9 +427,9 @@ d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, 
     return fail(D2SD_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws ? ws_bytes : 0,
                 plan.ws_bytes);
   if (args->total_nodes == 0) return ok();
-  hipEvent_t e0, e1;
-  timing_begin(&e0, &e1);
-  return hip_status(d2sd::launch_cascade_attention(*args, plan, ws, stream, e0, e1),
+  hipEvent_t ev[3];
+  timing_begin(ev);
+  return hip_status(d2sd::launch_cascade_attention(*args, plan, ws, stream, ev),
                     "cascade attention launch");
 }
 
@@ -383,9 +447,9 @@ d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStre
     return fail(D2SD_ERR_UNSUPPORTED, "the baseline streams at most %d context tokens per request", kMaxSplit);
   if (args->total_nodes == 0) return ok();
   const float scale = args->sm_scale > 0.0f ? args->sm_scale : 1.0f / sqrtf((float)args->head_dim);
-  hipEvent_t e0, e1;
-  timing_begin(&e0, &e1);
-  return hip_status(d2sd::launch_noncascade_attention(*args, scale, stream, e0, e1),
+  hipEvent_t ev[3];
+  timing_begin(ev);
+  return hip_status(d2sd::launch_noncascade_attention(*args, scale, stream, ev),
                     "non-cascade attention launch");
 }
 
@@ -450,11 +514,11 @@ d2sd_status d2sd_kernel_timing_enable(int enable) {
 
 d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms) {
   if (!launches || !total_ms) return fail(D2SD_ERR_INVALID_ARG, "output pointer is NULL");
-  std::vector<float> each;
-  const hipError_t err = collect_timings(&each);
+  std::vector<float> kern, merge;
+  const hipError_t err = collect_timings(&kern, &merge);
   double sum = 0.0;
-  for (float ms : each) sum += ms;
-  *launches = (int)each.size();
+  for (size_t i = 0; i < kern.size(); ++i) sum += (double)kern[i] + merge[i];
+  *launches = (int)kern.size();
   *total_ms = sum;
   return hip_status(err, "kernel timing");
 }
@@ -462,10 +526,23 @@ d2sd_status d2sd_kernel_timing_collect(int* launches, double* total_ms) {
 d2sd_status d2sd_kernel_timing_collect_each(int capacity, float* ms_each, int* launches) {
   if (!launches || capacity < 0 || (capacity > 0 && !ms_each))
     return fail(D2SD_ERR_INVALID_ARG, "launches is NULL, capacity < 0, or ms_each is NULL");
-  std::vector<float> each;
-  const hipError_t err = collect_timings(&each);
-  for (size_t i = 0; i < each.size() && i < (size_t)capacity; ++i) ms_each[i] = each[i];
-  *launches = (int)each.size();
+  std::vector<float> kern, merge;
+  const hipError_t err = collect_timings(&kern, &merge);
+  for (size_t i = 0; i < kern.size() && i < (size_t)capacity; ++i) ms_each[i] = kern[i] + merge[i];
+  *launches = (int)kern.size();
+  return hip_status(err, "kernel timing");
+}
+
+d2sd_status d2sd_kernel_timing_collect_parts(int capacity, float* kernel_ms, float* merge_ms, int* launches) {
+  if (!launches || capacity < 0 || (capacity > 0 && (!kernel_ms || !merge_ms)))
+    return fail(D2SD_ERR_INVALID_ARG, "launches is NULL, capacity < 0, or an output array is NULL");
+  std::vector<float> kern, merge;
+  const hipError_t err = collect_timings(&kern, &merge);
+  for (size_t i = 0; i < kern.size() && i < (size_t)capacity; ++i) {
+    kernel_ms[i] = kern[i];
+    merge_ms[i] = merge[i];
+  }
+  *launches = (int)kern.size();
   return hip_status(err, "kernel timing");
 }
 

@@ -1027,36 +1027,39 @@ Params make_params(const d2sd_attn_args& a, const AttnPlan& plan, void* ws) {
 }  // namespace
 
 hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& plan, void* ws,
-                                    hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+                                    hipStream_t stream, hipEvent_t (&ev)[3]) {
   const Params p = make_params(a, plan, ws);
   const int grid = (int)(((plan.items + 7) / 8) * 8);
-  if (ev0) (void)hipEventRecord(ev0, stream);
+  if (ev[0]) (void)hipEventRecord(ev[0], stream);
   if (a.dtype == D2SD_BF16)
     hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
   else
     hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
-  if (ev1) (void)hipEventRecord(ev1, stream);
+  if (ev[1]) (void)hipEventRecord(ev[1], stream);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || plan.n_ch_max <= 1) return e;
-  const int groups = merge_groups(plan.n_ch_max);
-  const long long chunks = merge_chunks_per_request(a.max_nodes, a.num_qo_heads, groups);
-  const dim3 mgrid((unsigned)(a.batch * chunks));
-  if (a.dtype == D2SD_BF16) {
-    if (groups > 1)
-      hipLaunchKernelGGL((split_merge_kernel<__bf16, 4>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
-    else
-      hipLaunchKernelGGL((split_merge_kernel<__bf16, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
-  } else {
-    if (groups > 1)
-      hipLaunchKernelGGL((split_merge_kernel<float, 4>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
-    else
-      hipLaunchKernelGGL((split_merge_kernel<float, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+  if (e == hipSuccess && plan.n_ch_max > 1) {
+    const int groups = merge_groups(plan.n_ch_max);
+    const long long chunks = merge_chunks_per_request(a.max_nodes, a.num_qo_heads, groups);
+    const dim3 mgrid((unsigned)(a.batch * chunks));
+    if (a.dtype == D2SD_BF16) {
+      if (groups > 1)
+        hipLaunchKernelGGL((split_merge_kernel<__bf16, 4>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+      else
+        hipLaunchKernelGGL((split_merge_kernel<__bf16, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+    } else {
+      if (groups > 1)
+        hipLaunchKernelGGL((split_merge_kernel<float, 4>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+      else
+        hipLaunchKernelGGL((split_merge_kernel<float, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
+    }
+    e = hipGetLastError();
   }
-  return hipGetLastError();
+  if (ev[2]) (void)hipEventRecord(ev[2], stream);
+  return e;
 }
 
 hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hipStream_t stream,
-                                       hipEvent_t ev0, hipEvent_t ev1) {
+                                       hipEvent_t (&ev)[3]) {
   AttnPlan plan{};
   plan.G = a.num_qo_heads / a.num_kv_heads;
   plan.split = 1 << 30;  // whole context in one pass
@@ -1067,12 +1070,13 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
   Params p = make_params(a, plan, nullptr);
   p.node_mode = 1;
   const int grid = (int)(((plan.items + 7) / 8) * 8);
-  if (ev0) (void)hipEventRecord(ev0, stream);
+  if (ev[0]) (void)hipEventRecord(ev[0], stream);
   if (a.dtype == D2SD_BF16)
     hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
   else
     hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
-  if (ev1) (void)hipEventRecord(ev1, stream);
+  if (ev[1]) (void)hipEventRecord(ev[1], stream);
+  if (ev[2]) (void)hipEventRecord(ev[2], stream);
   return hipGetLastError();
 }
 

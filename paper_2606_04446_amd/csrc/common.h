@@ -37,11 +37,13 @@ struct AttnPlan {
   float scale;       // softmax scale
 };
 
+// ev (nullable events): recorded before the main kernel, after it, and after
+// the split merge (right after the main kernel when there is none).
 hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& plan, void* ws,
-                                    hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+                                    hipStream_t stream, hipEvent_t (&ev)[3]);
 
 hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hipStream_t stream,
-                                       hipEvent_t ev0, hipEvent_t ev1);
+                                       hipEvent_t (&ev)[3]);
 
 hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,
                               const float* o_b, const float* lse_b, float* o_out, float* lse_out,

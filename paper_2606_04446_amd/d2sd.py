@@ -54,8 +54,12 @@ class AttnArgs(ctypes.Structure):
         ("max_pages", _c_int), ("mask_words", _c_int), ("kv_split", _c_int),
         ("q", _c_ptr), ("k_cache", _c_ptr), ("v_cache", _c_ptr), ("page_table", _c_ptr),
         ("ctx_len", _c_ptr), ("k_tree", _c_ptr), ("v_tree", _c_ptr), ("node_indptr", _c_ptr),
-        ("anc_mask", _c_ptr), ("out", _c_ptr), ("lse", _c_ptr),
+        ("anc_mask", _c_ptr), ("out", _c_ptr), ("lse", _c_ptr), ("node_indptr_host", _c_ptr),
     ]
+
+    def keep(self, *objs):
+        """Keep host arrays whose addresses the struct holds alive as long as it."""
+        self._keep = getattr(self, "_keep", ()) + objs
 
 
 def _sig(name, restype, *argtypes):
@@ -91,6 +95,8 @@ _sample = _sig("d2sd_sample_targets", _c_int, _c_int, _c_ptr, _c_int, _c_int, _c
 _timing_enable = _sig("d2sd_kernel_timing_enable", _c_int, _c_int)
 _timing_collect = _sig("d2sd_kernel_timing_collect", _c_int, _c_int_p, ctypes.POINTER(ctypes.c_double))
 _timing_each = _sig("d2sd_kernel_timing_collect_each", _c_int, _c_int, ctypes.POINTER(ctypes.c_float), _c_int_p)
+_timing_parts = _sig("d2sd_kernel_timing_collect_parts", _c_int, _c_int, ctypes.POINTER(ctypes.c_float),
+                     ctypes.POINTER(ctypes.c_float), _c_int_p)
 
 
 def _check(status: int, where: str):
@@ -258,8 +264,10 @@ def commit_accepted_kv(B: int, node_indptr, total_nodes: int, path_nodes, accept
 
 def attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse, *,
               total_nodes: int, max_nodes: int, max_ctx_len: int, stage: int = STAGE_CASCADE,
-              sm_scale: float = 0.0, kv_split: int = 0) -> AttnArgs:
-    """Fill a d2sd_attn_args from tensors (shapes as documented in the header)."""
+              sm_scale: float = 0.0, kv_split: int = 0, node_indptr_host=None) -> AttnArgs:
+    """Fill a d2sd_attn_args from tensors (shapes as documented in the header).
+    node_indptr_host: optional host copy of node_indptr (the automatic split
+    then counts the work items exactly)."""
     import torch
     dt = q.dtype
     code = {torch.float32: F32, torch.bfloat16: BF16}.get(dt)
@@ -293,6 +301,12 @@ def attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_ind
     a.anc_mask = _dev(anc_mask, "anc_mask", i32)
     a.out = _dev(out, "out", dt)
     a.lse = _dev(lse, "lse", torch.float32)
+    if node_indptr_host is not None:
+        ip = _host_i32(node_indptr_host)
+        if ip.shape != (a.batch + 1,):
+            raise ValueError(f"node_indptr_host must have {a.batch + 1} entries, got {ip.shape}")
+        a.node_indptr_host = ip.ctypes.data
+        a.keep(ip)
     return a
 
 
@@ -311,7 +325,7 @@ def cascade_kv_split(args: AttnArgs) -> int:
 def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask,
                              *, total_nodes: int, max_nodes: int, max_ctx_len: int, stage: int = STAGE_CASCADE,
                              sm_scale: float = 0.0, kv_split: int = 0, out=None, lse=None, workspace=None,
-                             want_lse: bool = True, stream=None):
+                             want_lse: bool = True, node_indptr_host=None, stream=None):
     """Verify attention; returns (out, lse). The workspace is allocated when not given."""
     import torch
     if out is None:
@@ -320,7 +334,7 @@ def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v
         lse = torch.empty(q.shape[:2], dtype=torch.float32, device=q.device)
     a = attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse,
                   total_nodes=total_nodes, max_nodes=max_nodes, max_ctx_len=max_ctx_len, stage=stage,
-                  sm_scale=sm_scale, kv_split=kv_split)
+                  sm_scale=sm_scale, kv_split=kv_split, node_indptr_host=node_indptr_host)
     need = cascade_workspace_size(a)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
@@ -418,7 +432,7 @@ def kernel_timing_enable(on: bool = True):
 
 
 def kernel_timing_collect():
-    """(launches, total_ms) of the context-streaming kernel since the last collect."""
+    """(calls, total_ms) of the attention operations (main kernel + split merge) since the last collect."""
     n = ctypes.c_int(0)
     ms = ctypes.c_double(0.0)
     _check(_timing_collect(ctypes.byref(n), ctypes.byref(ms)), "d2sd_kernel_timing_collect")
@@ -426,8 +440,18 @@ def kernel_timing_collect():
 
 
 def kernel_timing_collect_each(capacity: int = 4096):
-    """Durations (ms, launch order) of the context-streaming kernel since the last collect."""
+    """Durations (ms, call order) of the attention operations (main kernel + split merge) since the last collect."""
     buf = (ctypes.c_float * capacity)()
     n = ctypes.c_int(0)
     _check(_timing_each(capacity, buf, ctypes.byref(n)), "d2sd_kernel_timing_collect_each")
     return [float(buf[i]) for i in range(min(n.value, capacity))]
+
+
+def kernel_timing_collect_parts(capacity: int = 4096):
+    """(kernel_ms, merge_ms) lists, call order: the main kernel and the split merge of each call."""
+    kb = (ctypes.c_float * capacity)()
+    mb = (ctypes.c_float * capacity)()
+    n = ctypes.c_int(0)
+    _check(_timing_parts(capacity, kb, mb, ctypes.byref(n)), "d2sd_kernel_timing_collect_parts")
+    m = min(n.value, capacity)
+    return [float(kb[i]) for i in range(m)], [float(mb[i]) for i in range(m)]

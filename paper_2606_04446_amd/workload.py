@@ -1,9 +1,9 @@
 """Seeded synthetic inputs for one verify step (one attention layer).
 
 This module only draws random inputs; it contains no step of the verify
-computation. Tree sizes (``node_indptr``) and tree topology (``parent``) are
-passed in by the caller, who gets them from the library's host planner or from
-the oracle, so the generator does not duplicate tree construction.
+computation and builds no tree. Tree sizes (``node_indptr``) and tree
+topology (``parent``) are passed in by the caller, who gets them from the
+library's host planner and tree builder or from the oracle.
 
 Five workloads stand in for the paper's end-to-end runs (which use eight public
 benchmarks with trained drafters, not available here): they take the paper's
@@ -184,46 +184,6 @@ def draw_sub_branch_positions(layout: "Layout") -> np.ndarray:
             pk = int(layout.p[b, k])
             q[b, k] = int(rng.integers(pk + 1, B)) if pk < B - 1 else 0
     return q
-
-
-def parent_array(B: int, p_row: Sequence[int], q_row: Optional[Sequence[int]] = None,
-                 chains: int = 0) -> np.ndarray:
-    """Parent array (local indices, node 0 the anchor) of one request's tree,
-    as input for the parent-array tree builder:
-      chains > 0  `chains` independent chains of B-1 drafts under the anchor;
-      otherwise   the first-draft chain, one branch per re-anchor position p
-                  (ascending) hanging under the chain node at p - 1, and, when
-                  q_row is given, per branch a sub-branch hanging under the
-                  branch node at q - 1 (q > p; 0 = none), after all branches."""
-    par = [-1]
-    if chains > 0:
-        for _ in range(chains):
-            prev = 0
-            for _ in range(B - 1):
-                par.append(prev)
-                prev = len(par) - 1
-        return np.asarray(par, np.int32)
-    for j in range(1, B):
-        par.append(j - 1)
-    order = sorted(range(len(p_row)), key=lambda k: p_row[k])
-    at = {}                                     # (branch, position) -> node
-    for k in order:
-        pk = int(p_row[k])
-        prev = pk - 1
-        for pos in range(pk, B):
-            par.append(prev)
-            prev = len(par) - 1
-            at[(k, pos)] = prev
-    if q_row is not None:
-        for k in order:
-            qk = int(q_row[k])
-            if qk <= 0:
-                continue
-            prev = at[(k, qk - 1)] if qk - 1 >= int(p_row[k]) else qk - 1
-            for _ in range(qk, B):
-                par.append(prev)
-                prev = len(par) - 1
-    return np.asarray(par, np.int32)
 
 
 def draw_tokens(layout: Layout, node_indptr: np.ndarray, parent: np.ndarray,

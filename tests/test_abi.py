@@ -158,6 +158,12 @@ def test_commit_validation():
     assert call(hkv=1 << 26) == d2sd.ERR_UNSUPPORTED             # chunk index of a path past 2^31
     assert "exceeds" in d2sd.last_error()
     assert c(1, 16, 8, 128, 16, d2sd.BF16, 64, 64, 100, f, 10, f, f, f, f, f, None, f, f, None) == d2sd.ERR_INVALID_ARG
+    # K/V rows move in 16-byte chunks: every K/V pointer must be 16-byte aligned
+    for pos, name in ((13, "k_tree"), (14, "v_tree"), (17, "k_cache"), (18, "v_cache")):
+        args = [1, 16, 8, 128, 16, d2sd.BF16, 64, 64, 100, f, 10, f, f, f, f, f, f, f, f, None]
+        args[pos] = f + 8
+        assert c(*args) == d2sd.ERR_INVALID_ARG, name
+        assert name in d2sd.last_error() and "aligned" in d2sd.last_error()
 
 
 def test_sample_targets_validation():
@@ -236,6 +242,74 @@ def test_attention_null_pointers():
     assert d2sd._cascade(ctypes.byref(a), None, 0, None) == d2sd.ERR_WORKSPACE_TOO_SMALL
 
 
+def test_attention_alignment():
+    """Q, K/V and the output move in 16-byte chunks: a pointer off a 16-byte
+    boundary is rejected before any launch (the mask, page table and lse are
+    read in 4-byte units and need no more)."""
+    for name in ("q", "k_cache", "v_cache", "k_tree", "v_tree", "out"):
+        a = good_args(**{name: FAKE + 8})
+        assert d2sd._cascade(ctypes.byref(a), None, 0, None) == d2sd.ERR_INVALID_ARG, name
+        assert name in d2sd.last_error() and "aligned" in d2sd.last_error()
+        assert d2sd._noncascade(ctypes.byref(a), None) == d2sd.ERR_INVALID_ARG, name
+    # 4-byte aligned int arrays pass validation (the call stops at the missing workspace, before any launch)
+    a = good_args(page_table=FAKE + 4, ctx_len=FAKE + 4, anc_mask=FAKE + 4, node_indptr=FAKE + 4, kv_split=4096)
+    assert d2sd._cascade(ctypes.byref(a), None, 0, None) == d2sd.ERR_WORKSPACE_TOO_SMALL
+
+
+def _with_host_indptr(a, ip):
+    ip = np.ascontiguousarray(np.asarray(ip, np.int32))
+    a.node_indptr_host = ip.ctypes.data
+    a.keep(ip)
+    return a
+
+
+def test_node_indptr_host_validation():
+    ip = np.arange(33, dtype=np.int32) * 80            # 32 requests of 80 nodes
+    ok = _with_host_indptr(good_args(), ip)
+    assert ws_size(ok)[0] == d2sd.OK
+    for bad in (ip + 1, np.where(np.arange(33) == 32, 2559, ip), np.where(np.arange(33) == 5, 2000, ip)):
+        a = _with_host_indptr(good_args(), bad)
+        assert ws_size(a)[0] == d2sd.ERR_INVALID_ARG
+        assert "node_indptr_host" in d2sd.last_error()
+    big = np.concatenate([[0], np.cumsum([109] + [79] * 31)]).astype(np.int32)   # a request above max_nodes
+    assert ws_size(_with_host_indptr(good_args(total_nodes=int(big[-1])), big))[0] == d2sd.ERR_INVALID_ARG
+
+
+def _rounds_rule(groups: int, ctx: int, min_split: int = 256, resident: int = 768) -> int:
+    """The split length the planner documents for a grid of at least one round:
+    the split count s minimising ceil(g s / R) / s, more splits only for >= 3%."""
+    s_lo = max(1, -(-ctx // 32768))
+    s_hi = max(s_lo, ctx // min_split)
+    best_s, best = s_lo, -(-groups * s_lo // resident) / s_lo
+    for s in range(s_lo + 1, min(s_hi, 4 * s_lo) + 1):
+        t = -(-groups * s // resident) / s
+        if t < 0.97 * best:
+            best_s, best = s, t
+    per = -(-ctx // best_s)
+    return -(-per // 64) * 64
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_automatic_split_counts_rounds(cfg):
+    """Large grids: the split count comes from the resident rounds of the
+    exact work-item count (node offsets given on the host)."""
+    from paper_2606_04446_amd import workload as wl
+    lay = wl.draw_layout(cfg)
+    ip, W = d2sd.tree_plan(lay.spec.B, lay.K, lay.p)
+    n = np.diff(ip)
+    G = lay.spec.hq // lay.spec.hkv
+    groups = int((-(-(n * G) // 128)).sum()) * lay.spec.hkv
+    ctx = int(lay.ctx_len.max())
+    a = good_args(batch=lay.batch, num_qo_heads=lay.spec.hq, num_kv_heads=lay.spec.hkv, total_nodes=int(ip[-1]),
+                  max_nodes=int(n.max()), max_ctx_len=ctx, num_pages=lay.num_pages, max_pages=lay.max_pages,
+                  mask_words=W)
+    _with_host_indptr(a, ip)
+    split = d2sd.cascade_kv_split(a)
+    assert split == _rounds_rule(groups, ctx)
+    # the bench workloads: 768 work items (one round) at one split; 2800 (3.65 rounds) -> 3 splits (10.9 rounds)
+    assert (groups, -(-ctx // split)) == {4: (768, 1), 5: (2800, 3)}[cfg]
+
+
 def test_workspace_sizing_and_too_small():
     a = good_args(kv_split=4096)
     st, n = ws_size(a)
@@ -272,6 +346,10 @@ def test_timing_collect_empty():
     d2sd.kernel_timing_enable(False)
     assert d2sd.kernel_timing_collect() == (0, 0.0)
     assert d2sd.kernel_timing_collect_each() == []
+    assert d2sd.kernel_timing_collect_parts() == ([], [])
+    n = ctypes.c_int(-1)
+    assert d2sd._timing_parts(0, None, None, ctypes.byref(n)) == d2sd.OK and n.value == 0
+    assert d2sd._timing_parts(2, None, None, ctypes.byref(n)) == d2sd.ERR_INVALID_ARG
     n = ctypes.c_int(-1)
     assert d2sd._timing_each(0, None, ctypes.byref(n)) == d2sd.OK and n.value == 0
     assert d2sd._timing_each(-1, None, ctypes.byref(n)) == d2sd.ERR_INVALID_ARG

@@ -72,6 +72,29 @@ def test_record_and_use_traffic(tmp_path, monkeypatch):
     assert bench.measured_traffic(4, 0, 8192) is None
 
 
+def test_record_traffic_adds_the_split_merge(tmp_path, monkeypatch):
+    """With a split context the operation is the attention kernel plus the
+    split merge that reads the partial states back: both kernels' counters."""
+    rec_file = tmp_path / "traffic.json"
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(rec_file))
+    d = tmp_path / "t"
+    names = bench._workload_names()
+    line = {"dtype": "bf16", "config": {"workload": names[5], "kv_split": 10944}, "requested_kv_split": 0,
+            "roofline": {"splits": 3}}
+    os.makedirs(d)
+    (d / "fetch.log").write_text(json.dumps(line) + "\n")
+    write_counters(str(d / "fetch"), [(1, "cascade_bf16_kernel", "FETCH_SIZE", 1000.0),
+                                      (2, "split_merge_kernel<bf16, 1>", "FETCH_SIZE", 300.0)])
+    write_counters(str(d / "write"), [(1, "cascade_bf16_kernel", "WRITE_SIZE", 100.0),
+                                      (2, "split_merge_kernel<bf16, 1>", "WRITE_SIZE", 40.0)])
+    gib_kib = (1 << 30) / 1024.0
+    write_counters(str(d / "copy_fetch"), [(1, "__amd_rocclr_copyBuffer", "FETCH_SIZE", gib_kib)])
+    write_counters(str(d / "copy_write"), [(1, "__amd_rocclr_copyBuffer", "WRITE_SIZE", gib_kib)])
+    bench.record_traffic(str(d))
+    r = json.loads(rec_file.read_text())["config5"]
+    assert r["hbm_bytes_per_launch"] == (1300 + 140) * 1024
+
+
 def test_kernel_sha_is_stable():
     a, b = bench.kernel_sha(), bench.kernel_sha()
     assert a == b and len(a) == 16 and int(a, 16) >= 0
@@ -81,3 +104,22 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_parent_arrays_match_oracle_constructions():
+    """The benchmark's parent arrays (inputs of the parent-array tree builder)
+    are the oracle's canonical, third-level and resample trees."""
+    from oracle.tree import build_tree, resample_parents, third_level_parents
+
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        B = int(rng.integers(3, 40))
+        K = int(rng.integers(0, min(B - 2, 8) + 1))
+        p = rng.choice(np.arange(1, B - 1), size=K, replace=False).tolist()
+        q = [int(rng.integers(pk + 1, B)) for pk in p]
+        assert bench.bench_parent_array(B, p).tolist() == build_tree(B, p).parent
+        if K:
+            order = np.argsort(p)
+            assert bench.bench_parent_array(B, p, q).tolist() == third_level_parents(B, sorted(p), [q[i] for i in order])
+        c = int(rng.integers(1, 5))
+        assert bench.bench_parent_array(B, [], chains=c).tolist() == resample_parents(B, c)

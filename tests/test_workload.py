@@ -76,22 +76,3 @@ def test_token_model_matches_closed_form():
     base = np.repeat(ip[:-1], np.diff(ip))
     match = draft[nonroot] == argmax[(base + parent)[nonroot]]
     assert abs(match.mean() - 0.7) < 0.01
-
-
-def test_parent_arrays_match_oracle_constructions():
-    """The generator's parent arrays (bench inputs for the parent-array tree
-    builder) are the oracle's canonical, third-level and resample trees."""
-    from oracle.tree import build_tree, resample_parents, third_level_parents
-
-    rng = np.random.default_rng(0)
-    for _ in range(200):
-        B = int(rng.integers(3, 40))
-        K = int(rng.integers(0, min(B - 2, 8) + 1))
-        p = rng.choice(np.arange(1, B - 1), size=K, replace=False).tolist()
-        q = [int(rng.integers(pk + 1, B)) for pk in p]
-        assert wl.parent_array(B, p).tolist() == build_tree(B, p).parent
-        if K:
-            order = np.argsort(p)
-            assert wl.parent_array(B, p, q).tolist() == third_level_parents(B, sorted(p), [q[i] for i in order])
-        c = int(rng.integers(1, 5))
-        assert wl.parent_array(B, [], chains=c).tolist() == resample_parents(B, c)
