@@ -62,6 +62,8 @@ def parse():
     ap.add_argument("--profile-stage", choices=["cascade", "prefix", "tree"],
                     help="only run W + K attention calls of this stage on the workload (no step, no oracle), "
                          "e.g. the tree-suffix tiles alone for MFMA counters; prints a short JSON line")
+    ap.add_argument("--prefix-stage", action="store_true",
+                    help="also time the attention call with the context keys only (STAGE_PREFIX)")
     ap.add_argument("--tree", choices=["canonical", "third_level", "resample"], default="canonical",
                     help="tree shape: the canonical chain-plus-branches tree (default), the third-level cascade "
                          "(a sub-branch inside every branch) or K+1 resampled chains, the latter two built from "
@@ -126,6 +128,13 @@ def measured_traffic(config: int, kv_split: int, resolved_split: int):
     return r.get("hbm_bytes_per_launch")
 
 
+def kernel_name_matches(name: str, kernel: str) -> bool:
+    """Whether a demangled kernel name is `kernel` (as a whole identifier:
+    "cascade_bf16_kernel" does not match "noncascade_bf16_kernel")."""
+    import re
+    return re.search(r"(?<![A-Za-z0-9_])" + re.escape(kernel) + r"(?![A-Za-z0-9_])", name) is not None
+
+
 def _counter_per_dispatch(csv_dir: str, kernel: str, counter: str) -> float:
     """Mean over dispatches of `kernel` of the counter's value (summed over the
     rows of each dispatch) in a rocprofv3 counter-collection CSV."""
@@ -139,7 +148,7 @@ def _counter_per_dispatch(csv_dir: str, kernel: str, counter: str) -> float:
     for path in paths:
         with open(path) as f:
             for r in csv.DictReader(f):
-                if kernel in r["Kernel_Name"] and r["Counter_Name"] == counter:
+                if kernel_name_matches(r["Kernel_Name"], kernel) and r["Counter_Name"] == counter:
                     per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
     if not per:
         raise ValueError(f"no {counter} rows for {kernel} under {csv_dir}")
@@ -161,8 +170,8 @@ def record_traffic(d: str):
         fetch += _counter_per_dispatch(os.path.join(d, "fetch"), "split_merge_kernel", "FETCH_SIZE")
         write += _counter_per_dispatch(os.path.join(d, "write"), "split_merge_kernel", "WRITE_SIZE")
     copy_kib = (1 << 30) / 1024.0
-    f_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_fetch"), "copyBuffer", "FETCH_SIZE")
-    w_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_write"), "copyBuffer", "WRITE_SIZE")
+    f_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_fetch"), "__amd_rocclr_copyBuffer", "FETCH_SIZE")
+    w_fac = copy_kib / _counter_per_dispatch(os.path.join(d, "copy_write"), "__amd_rocclr_copyBuffer", "WRITE_SIZE")
     cfg = bench["config"]
     cfg_num = next(k for k, v in _workload_names().items() if v == cfg["workload"])
     rec = {}
@@ -383,10 +392,14 @@ def main():
                                                                  np.diff(node_indptr)).sum())
                                                  + (tree_keys if stage == d2sd.STAGE_CASCADE else 0.0))
         k_ms = float(np.mean(kern))
-        print(json.dumps({"profile_stage": args.profile_stage, "workload": spec.name, "calls": len(kern),
+        splits = n_splits if stage != d2sd.STAGE_TREE else 1
+        # the keys read by --record-traffic: dtype, config, requested_kv_split, roofline.splits
+        print(json.dumps({"profile_stage": args.profile_stage, "dtype": spec.dtype, "calls": len(kern),
+                          "config": {"workload": spec.name, "kv_split": kv_split, "tree": args.tree},
+                          "requested_kv_split": args.kv_split, "roofline": {"splits": splits},
                           "kernel_ms": round(k_ms, 4), "merge_ms": round(float(np.mean(merge)), 4),
-                          "algorithmic_flop_per_call": flops, "tflops": round(flops / (k_ms / 1e3) / 1e12, 3),
-                          "kv_split": kv_split}), flush=True)
+                          "algorithmic_flop_per_call": flops, "tflops": round(flops / (k_ms / 1e3) / 1e12, 3)}),
+              flush=True)
         return
 
     def step():
@@ -448,21 +461,23 @@ def main():
     kern_ms = float(np.mean(kern_cold))
     merge_ms = float(np.mean(merge_cold))
 
-    # The prefix stage alone (context keys only, no tree tiles): the time
-    # that the prefix K/V bandwidth is also quoted against.
-    out_p, lse_p = torch.empty_like(out), torch.empty_like(lse)
-    for _ in range(args.warmup):
-        attention(d2sd.STAGE_PREFIX, out_p, lse_p)
-    torch.cuda.synchronize()
-    d2sd.kernel_timing_collect_parts()
-    d2sd.kernel_timing_enable(True)
-    for _ in range(args.steps):
-        attention(d2sd.STAGE_PREFIX, out_p, lse_p)
-    torch.cuda.synchronize()
-    d2sd.kernel_timing_enable(False)
-    pk, pm = d2sd.kernel_timing_collect_parts()
-    prefix_ms = float(np.mean(pk)) + float(np.mean(pm))
-    del out_p, lse_p
+    # The prefix stage alone (context keys only, no tree tiles), on request:
+    # the time that the prefix K/V bandwidth can also be quoted against.
+    prefix_ms = None
+    if args.prefix_stage:
+        out_p, lse_p = torch.empty_like(out), torch.empty_like(lse)
+        for _ in range(args.warmup):
+            attention(d2sd.STAGE_PREFIX, out_p, lse_p)
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_collect_parts()
+        d2sd.kernel_timing_enable(True)
+        for _ in range(args.steps):
+            attention(d2sd.STAGE_PREFIX, out_p, lse_p)
+        torch.cuda.synchronize()
+        d2sd.kernel_timing_enable(False)
+        pk, pm = d2sd.kernel_timing_collect_parts()
+        prefix_ms = float(np.mean(pk)) + float(np.mean(pm))
+        del out_p, lse_p
 
     # The same step captured once in a HIP graph and replayed (the step
     # allocates nothing and issues no memset, so it can be captured as it is).
@@ -539,9 +554,9 @@ def main():
                           "MFMA peak"),
         "prefix_kv_gbps": round(gbps, 1),
         "prefix_kv_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
-        "prefix_stage": {"ms": round(prefix_ms, 4),
-                         "prefix_kv_gbps": round(prefix_bytes / (prefix_ms / 1e3) / 1e9, 1),
-                         "prefix_kv_hbm_frac": round(prefix_bytes / (prefix_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)},
+        "prefix_stage": None if prefix_ms is None else {
+            "ms": round(prefix_ms, 4), "prefix_kv_gbps": round(prefix_bytes / (prefix_ms / 1e3) / 1e9, 1),
+            "prefix_kv_hbm_frac": round(prefix_bytes / (prefix_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)},
         "attn_tflops": round(tflops, 2),
         "attn_mfma_frac": round(tflops / MFMA_PEAK_TFLOPS[spec.dtype], 4),
         "attn_ms": round(op_ms, 4),

@@ -38,6 +38,7 @@ std::mutex g_timing_mu;
 bool g_timing_on = false;
 struct TimedLaunch {
   hipEvent_t e0, e1, e2;  // before the main kernel, after it, after the split merge
+  bool merged;            // e2 was recorded (the call launched a split merge)
 };
 std::vector<TimedLaunch> g_timing_pending;
 std::vector<hipEvent_t> g_event_pool;
@@ -64,14 +65,23 @@ void timing_begin(hipEvent_t (&ev)[3]) {
       if (e) g_event_pool.push_back(e);
       e = nullptr;
     }
-    return;
   }
-  g_timing_pending.push_back({ev[0], ev[1], ev[2]});
 }
 
-// Wait for every recorded launch and return, in launch order, the main
-// kernel's duration and the split merge's (ms; 0 when the call had no
-// merge); recycle the events and clear the record.
+// Record a timed call after its launches (merged: ev[2] was recorded), or
+// return the events to the pool when the launch failed.
+void timing_end(hipEvent_t (&ev)[3], bool launched, bool merged) {
+  if (!ev[0]) return;
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  if (launched)
+    g_timing_pending.push_back({ev[0], ev[1], ev[2], merged});
+  else
+    for (auto& e : ev) g_event_pool.push_back(e);
+}
+
+// Wait for every recorded call and return, in call order, the main kernel's
+// duration and the split merge's (ms; 0 when the call had no merge);
+// recycle the events and clear the record.
 hipError_t collect_timings(std::vector<float>* kernel, std::vector<float>* merge) {
   std::vector<TimedLaunch> pend;
   {
@@ -83,9 +93,9 @@ hipError_t collect_timings(std::vector<float>* kernel, std::vector<float>* merge
   merge->reserve(pend.size());
   for (auto& t : pend) {
     float k_ms = 0.0f, m_ms = 0.0f;
-    hipError_t e = hipEventSynchronize(t.e2);
+    hipError_t e = hipEventSynchronize(t.merged ? t.e2 : t.e1);
     if (e == hipSuccess) e = hipEventElapsedTime(&k_ms, t.e0, t.e1);
-    if (e == hipSuccess) e = hipEventElapsedTime(&m_ms, t.e1, t.e2);
+    if (e == hipSuccess && t.merged) e = hipEventElapsedTime(&m_ms, t.e1, t.e2);
     if (e != hipSuccess && err == hipSuccess) err = e;
     kernel->push_back(k_ms);
     merge->push_back(m_ms);
@@ -429,8 +439,9 @@ d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, 
   if (args->total_nodes == 0) return ok();
   hipEvent_t ev[3];
   timing_begin(ev);
-  return hip_status(d2sd::launch_cascade_attention(*args, plan, ws, stream, ev),
-                    "cascade attention launch");
+  const hipError_t e = d2sd::launch_cascade_attention(*args, plan, ws, stream, ev);
+  timing_end(ev, e == hipSuccess, plan.n_ch_max > 1);
+  return hip_status(e, "cascade attention launch");
 }
 
 d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStream_t stream) {
@@ -449,8 +460,9 @@ d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStre
   const float scale = args->sm_scale > 0.0f ? args->sm_scale : 1.0f / sqrtf((float)args->head_dim);
   hipEvent_t ev[3];
   timing_begin(ev);
-  return hip_status(d2sd::launch_noncascade_attention(*args, scale, stream, ev),
-                    "non-cascade attention launch");
+  const hipError_t e = d2sd::launch_noncascade_attention(*args, scale, stream, ev);
+  timing_end(ev, e == hipSuccess, false);
+  return hip_status(e, "non-cascade attention launch");
 }
 
 d2sd_status d2sd_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,

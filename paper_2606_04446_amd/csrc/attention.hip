@@ -59,7 +59,6 @@ struct Params {
   int batch, hq, hkv, G, stage;
   int total_nodes, max_nodes, max_ctx, num_pages, max_pages, mask_words;
   int split, n_ch_max, n_rg_max, items;
-  int node_mode;  // 1: one workgroup per (request, node, KV head), no context sharing
   float c2;  // sm_scale * log2(e)
 };
 
@@ -216,8 +215,10 @@ __device__ __forceinline__ void store_out<float>(float* dst, const float* v) {
   *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
+// kNode: the non-cascade baseline, one workgroup per (request, node, KV
+// head) streaming the whole context for that node's query heads.
+template <typename T, bool kNode>
+__device__ __forceinline__ void attention_body(const Params& p) {
   using C = Tile<T>;
   using QF = typename Frag<T>::Q;
   constexpr int KT = C::KT;
@@ -234,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
   if (item >= p.items) return;
   int rest = item;
   int rg = 0, ch = 0, n_sel = 0;
-  if (p.node_mode) {
+  if (kNode) {
     n_sel = rest % p.max_nodes; rest /= p.max_nodes;
   } else {
     rg = rest % p.n_rg_max; rest /= p.n_rg_max;
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
   const int Mb = Nb * p.G;
   // rows [r_lo, r_hi) of the (request, KV head) column block owned by this workgroup
   int r_lo, r_hi;
-  if (p.node_mode) {
+  if (kNode) {
     if (n_sel >= Nb) return;
     r_lo = n_sel * p.G;
     r_hi = r_lo + p.G;
@@ -424,6 +425,15 @@ __global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
       }
     }
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void cascade_attention_kernel(Params p) {
+  attention_body<T, false>(p);
+}
+template <typename T>
+__global__ __launch_bounds__(kThreads) void noncascade_attention_kernel(Params p) {
+  attention_body<T, true>(p);
 }
 
 // ---------------------------------------------------------------------------
@@ -704,8 +714,8 @@ __device__ __forceinline__ uint64_t tree_bits(const Params& p, int node_base, in
   return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
-__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
-void cascade_bf16_kernel(Params p) {
+template <bool kNode>
+__device__ __forceinline__ void bf16_attention_body(const Params& p) {
   constexpr int GROUP_ROWS = bf::WAVES * kRowsPerTile;
   // the two stages of the K/V ring
   __shared__ __attribute__((aligned(1024))) char sk0[bf::TILE_BYTES], sv0[bf::TILE_BYTES];
@@ -718,7 +728,7 @@ void cascade_bf16_kernel(Params p) {
   if (item >= p.items) return;
   int rest = item;
   int rg = 0, ch = 0, n_sel = 0;
-  if (p.node_mode) {
+  if (kNode) {
     n_sel = rest % p.max_nodes; rest /= p.max_nodes;
   } else {
     rg = rest % p.n_rg_max; rest /= p.n_rg_max;
@@ -730,7 +740,7 @@ void cascade_bf16_kernel(Params p) {
   const int Nb = clampi(p.node_indptr[b + 1] - node_base, 0, min(p.max_nodes, p.total_nodes - node_base));
   const int Mb = Nb * p.G;
   int r_lo, r_hi;
-  if (p.node_mode) {
+  if (kNode) {
     if (n_sel >= Nb) return;
     r_lo = n_sel * p.G;
     r_hi = r_lo + p.G;
@@ -889,6 +899,16 @@ void cascade_bf16_kernel(Params p) {
       p.ws_l[prow] = l_all;
     }
   }
+}
+
+__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+void cascade_bf16_kernel(Params p) {
+  bf16_attention_body<false>(p);
+}
+// The non-cascade baseline: the same body, one workgroup per (request, node, KV head).
+__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+void noncascade_bf16_kernel(Params p) {
+  bf16_attention_body<true>(p);
 }
 
 // Log-sum-exp reduction of the split partials of every output row (rows of
@@ -1053,8 +1073,8 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
         hipLaunchKernelGGL((split_merge_kernel<float, 1>), mgrid, dim3(kThreads), 0, stream, p, (int)chunks);
     }
     e = hipGetLastError();
+    if (ev[2]) (void)hipEventRecord(ev[2], stream);
   }
-  if (ev[2]) (void)hipEventRecord(ev[2], stream);
   return e;
 }
 
@@ -1067,16 +1087,14 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
   plan.n_rg_max = 1;
   plan.items = (long long)a.batch * a.num_kv_heads * a.max_nodes;
   plan.scale = scale;
-  Params p = make_params(a, plan, nullptr);
-  p.node_mode = 1;
+  const Params p = make_params(a, plan, nullptr);
   const int grid = (int)(((plan.items + 7) / 8) * 8);
   if (ev[0]) (void)hipEventRecord(ev[0], stream);
   if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
+    hipLaunchKernelGGL(noncascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
   else
-    hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(noncascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
   if (ev[1]) (void)hipEventRecord(ev[1], stream);
-  if (ev[2]) (void)hipEventRecord(ev[2], stream);
   return hipGetLastError();
 }
 

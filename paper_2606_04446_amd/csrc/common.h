@@ -37,8 +37,9 @@ struct AttnPlan {
   float scale;       // softmax scale
 };
 
-// ev (nullable events): recorded before the main kernel, after it, and after
-// the split merge (right after the main kernel when there is none).
+// ev (nullable events): ev[0] is recorded before the main kernel, ev[1]
+// after it, and ev[2] after the split merge; ev[2] is left unrecorded when
+// the call launches no merge (the caller then times the main kernel only).
 hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& plan, void* ws,
                                     hipStream_t stream, hipEvent_t (&ev)[3]);
 

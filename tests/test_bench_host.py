@@ -34,9 +34,9 @@ def write_counters(d, rows):
 
 def test_counter_per_dispatch_sums_rows_then_averages(tmp_path):
     d = str(tmp_path / "c")
-    write_counters(d, [(1, "k_cascade", "FETCH_SIZE", 10), (1, "k_cascade", "FETCH_SIZE", 5),
-                       (2, "k_cascade", "FETCH_SIZE", 25), (3, "other", "FETCH_SIZE", 1000),
-                       (2, "k_cascade", "WRITE_SIZE", 7)])
+    write_counters(d, [(1, "ns::cascade(P)", "FETCH_SIZE", 10), (1, "ns::cascade(P)", "FETCH_SIZE", 5),
+                       (2, "ns::cascade(P)", "FETCH_SIZE", 25), (3, "other", "FETCH_SIZE", 1000),
+                       (4, "ns::noncascade(P)", "FETCH_SIZE", 999), (2, "ns::cascade(P)", "WRITE_SIZE", 7)])
     assert bench._counter_per_dispatch(d, "cascade", "FETCH_SIZE") == 20.0   # (15 + 25) / 2
     with pytest.raises(ValueError):
         bench._counter_per_dispatch(d, "cascade", "TCC_HIT")
@@ -93,6 +93,15 @@ def test_record_traffic_adds_the_split_merge(tmp_path, monkeypatch):
     bench.record_traffic(str(d))
     r = json.loads(rec_file.read_text())["config5"]
     assert r["hbm_bytes_per_launch"] == (1300 + 140) * 1024
+
+
+def test_kernel_names_match_whole_identifiers():
+    m = bench.kernel_name_matches
+    assert m("d2sd::(anonymous namespace)::cascade_bf16_kernel(d2sd::(anonymous namespace)::Params)",
+             "cascade_bf16_kernel")
+    assert not m("d2sd::(anonymous namespace)::noncascade_bf16_kernel(Params)", "cascade_bf16_kernel")
+    assert m("void split_merge_kernel<__bf16, 4>(Params, int)", "split_merge_kernel")
+    assert not m("cascade_bf16_kernel_v2", "cascade_bf16_kernel")
 
 
 def test_kernel_sha_is_stable():
