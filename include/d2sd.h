@@ -292,6 +292,26 @@ d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, 
                                           hipStream_t stream);
 
 /*
+ * Device. The same verify attention as d2sd_cascade_verify_attention, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): it takes no
+ * workspace and allocates nothing. The split partial states live in a static
+ * device scratch of the library, 64 MiB (67,108,864 bytes) per GPU, held on
+ * every GPU the library runs on until the process ends. With an explicit
+ * kv_split whose partial states exceed 64 MiB it returns
+ * D2SD_ERR_WORKSPACE_TOO_SMALL; with the automatic split (kv_split = 0) it
+ * takes the automatic plan, or, when that does not fit, the fewest-split
+ * longer splits that do (the results then differ from the workspace entry
+ * point's by summation order only), and returns D2SD_ERR_WORKSPACE_TOO_SMALL
+ * if even ceil(max_ctx_len / 32768) splits do not fit. The scratch holds
+ * nothing that must start at zero; every call on one GPU shares it and
+ * leaves its last contents there, so calls that overlap on one GPU (two
+ * streams, two host threads) race. Arguments, errors and outputs otherwise
+ * as for d2sd_cascade_verify_attention.
+ */
+d2sd_status d2sd_cascade_verify_attention_noalloc(const d2sd_attn_args* args, hipStream_t stream);
+
+/*
  * Device. Log-sum-exp merge of two attention states over disjoint key sets
  * (the cascade merge): with m = max(lse_a, lse_b), wa = exp(lse_a - m),
  * wb = exp(lse_b - m): o = (wa*o_a + wb*o_b)/(wa+wb), lse = m + ln(wa+wb).

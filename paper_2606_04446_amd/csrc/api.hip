@@ -444,6 +444,45 @@ d2sd_status d2sd_cascade_verify_attention(const d2sd_attn_args* args, void* ws, 
   return hip_status(e, "cascade attention launch");
 }
 
+d2sd_status d2sd_cascade_verify_attention_noalloc(const d2sd_attn_args* args, hipStream_t stream) {
+  d2sd_status s = validate_attn(args, true);
+  if (s) return s;
+  d2sd::AttnPlan plan;
+  if ((s = make_plan(args, &plan))) return s;
+  if (plan.ws_bytes > d2sd::kScratchBytes) {
+    if (args->kv_split > 0)
+      return fail(D2SD_ERR_WORKSPACE_TOO_SMALL,
+                  "kv_split %d needs %zu bytes of partial states; the static scratch holds %zu "
+                  "(use a longer kv_split, or the workspace entry point)",
+                  args->kv_split, plan.ws_bytes, d2sd::kScratchBytes);
+    // automatic split: fewer, longer splits until the partial states fit
+    d2sd_attn_args fit = *args;
+    const int ctx = args->max_ctx_len;
+    const int s_lo = max(1, (ctx + kMaxSplit - 1) / kMaxSplit);
+    bool found = false;
+    for (int n = plan.n_ch_max - 1; n >= s_lo && !found; --n) {
+      fit.kv_split = min(kMaxSplit, ((ctx + n - 1) / n + 63) / 64 * 64);
+      if ((s = make_plan(&fit, &plan))) return s;
+      found = plan.ws_bytes <= d2sd::kScratchBytes;
+    }
+    if (!found)
+      return fail(D2SD_ERR_WORKSPACE_TOO_SMALL,
+                  "the partial states of %d context splits need %zu bytes; the static scratch holds %zu",
+                  plan.n_ch_max, plan.ws_bytes, d2sd::kScratchBytes);
+  }
+  if (args->total_nodes == 0) return ok();
+  void* ws = nullptr;
+  if (plan.ws_bytes > 0) {
+    const hipError_t e = d2sd::scratch_address(&ws);
+    if (e != hipSuccess) return hip_status(e, "static scratch address");
+  }
+  hipEvent_t ev[3];
+  timing_begin(ev);
+  const hipError_t e = d2sd::launch_cascade_attention(*args, plan, ws, stream, ev);
+  timing_end(ev, e == hipSuccess, plan.n_ch_max > 1);
+  return hip_status(e, "cascade attention launch");
+}
+
 d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStream_t stream) {
   d2sd_status s = validate_attn(args, true);
   if (s) return s;

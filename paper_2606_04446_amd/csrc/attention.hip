@@ -30,6 +30,8 @@
 // more than 2^8, and skips masking on interior context tiles.
 #include <math.h>
 
+#include <mutex>
+
 #include "common.h"
 
 namespace d2sd {
@@ -1096,6 +1098,34 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
     hipLaunchKernelGGL(noncascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
   if (ev[1]) (void)hipEventRecord(ev[1], stream);
   return hipGetLastError();
+}
+
+// ---- static scratch of the allocation-free entry point -------------------
+// The split partial states of d2sd_cascade_verify_attention_noalloc live in
+// this file-scope device array instead of a caller workspace. Each GPU the
+// library runs on holds its own copy until the process ends. In host code
+// `scratch` names a host-side stand-in, never the device memory: kernels get
+// the address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+hipError_t scratch_address(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // with `dev` current: its own copy
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,

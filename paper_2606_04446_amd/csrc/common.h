@@ -46,6 +46,12 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
 hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hipStream_t stream,
                                        hipEvent_t (&ev)[3]);
 
+// Size of the static device scratch that backs the allocation-free attention
+// entry point (split partial states), and its device address on the current
+// device (looked up once per device).
+constexpr size_t kScratchBytes = 64ull << 20;
+hipError_t scratch_address(void** out);
+
 hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const float* lse_a,
                               const float* o_b, const float* lse_b, float* o_out, float* lse_out,
                               hipStream_t stream);

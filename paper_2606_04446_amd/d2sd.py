@@ -86,6 +86,7 @@ _ws_size = _sig("d2sd_cascade_workspace_size", _c_int, ctypes.POINTER(AttnArgs),
 _kv_split = _sig("d2sd_cascade_kv_split", _c_int, ctypes.POINTER(AttnArgs), _c_int_p)
 _cascade = _sig("d2sd_cascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr, _c_size, _c_ptr)
 _noncascade = _sig("d2sd_noncascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr)
+_cascade_noalloc = _sig("d2sd_cascade_verify_attention_noalloc", _c_int, ctypes.POINTER(AttnArgs), _c_ptr)
 _merge = _sig("d2sd_merge_state", _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
               _c_ptr)
 _accept = _sig("d2sd_accept_path", _c_int, _c_int, _c_int, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
@@ -341,6 +342,20 @@ def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v
     ws_ptr = _dev(workspace, "workspace") if workspace is not None else None
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(_cascade(ctypes.byref(a), ws_ptr, ws_len, _stream(stream)), "d2sd_cascade_verify_attention")
+    return out, lse
+
+
+def cascade_verify_attention_noalloc(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr,
+                                     anc_mask, *, total_nodes: int, max_nodes: int, max_ctx_len: int,
+                                     stage: int = STAGE_CASCADE, sm_scale: float = 0.0, kv_split: int = 0, out,
+                                     lse=None, node_indptr_host=None, stream=None):
+    """Verify attention through the allocation-free entry point: the caller
+    passes the outputs, the split partial states use the library's static
+    device scratch. Returns (out, lse)."""
+    a = attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse,
+                  total_nodes=total_nodes, max_nodes=max_nodes, max_ctx_len=max_ctx_len, stage=stage,
+                  sm_scale=sm_scale, kv_split=kv_split, node_indptr_host=node_indptr_host)
+    _check(_cascade_noalloc(ctypes.byref(a), _stream(stream)), "d2sd_cascade_verify_attention_noalloc")
     return out, lse
 
 
