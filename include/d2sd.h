@@ -248,6 +248,9 @@ typedef struct d2sd_attn_args {
   int max_pages;     /* row stride of page_table */
   int mask_words;    /* row stride of anc_mask; >= ceil(max_nodes/32) */
   int kv_split;      /* context tokens per split, multiple of 64; 0 = automatic */
+  int row_group;     /* bf16 query rows per workgroup: 0 = automatic, 128 (4 waves,
+                        three workgroups per CU) or 384 (12 waves sharing one K/V
+                        ring, one workgroup per CU); fp32 always takes 128 */
   const void* q;
   const void* k_cache;
   const void* v_cache;
@@ -279,12 +282,19 @@ d2sd_status d2sd_cascade_workspace_size(const d2sd_attn_args* args, size_t* byte
 d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split);
 
 /*
+ * Host. The query rows per workgroup (128 or 384) the attention call will use
+ * for `args` (args->row_group if nonzero, else the automatic choice).
+ */
+d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows);
+
+/*
  * Device. Verify attention (see d2sd_attn_args). The M = N_b * G query rows
- * of a (request, KV head) are cut into row groups of 128 (bf16); every
- * context page slab is streamed once per (context split, row group) and
- * reused by all 128 rows of the group, i.e. by all G query heads of the
- * group's tree nodes. The row groups of one split run as neighbouring
- * workgroups on one XCD, so that later readers of a slab mostly hit its L2.
+ * of a (request, KV head) are cut into row groups of 128 or 384 (bf16,
+ * d2sd_cascade_row_group); every context page slab is streamed once per
+ * (context split, row group) and reused by all rows of the group, i.e. by
+ * all G query heads of the group's tree nodes. The row groups of one split
+ * run as neighbouring workgroups on one XCD, so that later readers of a slab
+ * mostly hit its L2.
  * ws: device workspace of ws_bytes >= d2sd_cascade_workspace_size(args) (may
  * be NULL when that size is 0). Concurrent calls must not share a workspace.
  */

@@ -159,6 +159,10 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
   if (a->kv_split < 0 || a->kv_split % 64 || a->kv_split > kMaxSplit)
     return fail(D2SD_ERR_INVALID_ARG, "kv_split %d must be 0 or a multiple of 64 in [64, %d]", a->kv_split,
                 kMaxSplit);
+  if (a->row_group != 0 && a->row_group != d2sd::kBf16Waves * d2sd::kRowsPerTile &&
+      a->row_group != d2sd::kBf16WideWaves * d2sd::kRowsPerTile)
+    return fail(D2SD_ERR_INVALID_ARG, "row_group %d must be 0, %d or %d", a->row_group,
+                d2sd::kBf16Waves * d2sd::kRowsPerTile, d2sd::kBf16WideWaves * d2sd::kRowsPerTile);
   if (a->stage != D2SD_STAGE_PREFIX && a->mask_words < (a->max_nodes + 31) / 32)
     return fail(D2SD_ERR_INVALID_ARG, "mask_words %d too small for max_nodes %d", a->mask_words,
                 a->max_nodes);
@@ -187,10 +191,10 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
   return D2SD_OK;
 }
 
-// Row groups (work items) of one context split over the batch: exact when the
-// host copy of the node offsets is given, else from the mean tree size.
-long long groups_per_split(const d2sd_attn_args* a, int G) {
-  const int rows_per_group = d2sd::group_rows(a->dtype);
+// Row groups (work items) of one context split over the batch, for groups of
+// rows_per_group query rows: exact when the host copy of the node offsets is
+// given, else from the mean tree size.
+long long groups_per_split(const d2sd_attn_args* a, int G, int rows_per_group) {
   long long groups = 0;
   if (a->node_indptr_host) {
     for (int b = 0; b < a->batch; ++b) {
@@ -204,54 +208,99 @@ long long groups_per_split(const d2sd_attn_args* a, int G) {
   return max(1ll, groups * a->num_kv_heads);
 }
 
-// Context tokens per split (automatic choice). R = resident workgroups (three
-// per CU for the 4-wave bf16 kernel, one otherwise) and g = row groups per
-// split. When one split already gives at least R work items, work items of
-// equal length run in ceil(g s / R) rounds of resident workgroups, each 1/s
-// of a context long, so the kernel takes time in proportion to
-// ceil(g s / R) / s: the split count s minimising it is taken, a larger s
-// only for a gain of at least 3% (every split adds a partial state that the
-// merge reads back). Smaller grids take about two rounds of work items. No
-// split is shorter than the dtype's minimum (the partial state of a split
+// Relative kernel time of g row groups per split at s splits with R resident
+// workgroups: work items of equal length (1/s of a context) run in
+// ceil(g s / R) rounds of resident workgroups.
+double rounds_time(long long g, long long R, int s) { return (double)((g * s + R - 1) / R) / s; }
+
+// The split count in [s_lo, s_hi] minimising rounds_time, a larger count only
+// for a gain of at least 3% (every split adds a partial state that the merge
+// reads back).
+int best_splits(long long g, long long R, int s_lo, int s_hi, double* t) {
+  int best_s = s_lo;
+  double best = rounds_time(g, R, s_lo);
+  for (int s = s_lo + 1; s <= min(s_hi, 4 * s_lo); ++s) {
+    const double ts = rounds_time(g, R, s);
+    if (ts < 0.97 * best) {
+      best = ts;
+      best_s = s;
+    }
+  }
+  *t = best;
+  return best_s;
+}
+
+// Measured speed of the twelve-wave bf16 shape against the four-wave one for
+// the same filled waves (one context read per 384 rows instead of per 128):
+// 8% on the 32-request, 16k-context workload.
+constexpr double kWideGain = 1.08;
+
+// Workgroup shape and context tokens per split. R = resident workgroups:
+// three 4-wave or one 12-wave bf16 workgroup per CU, one fp32 workgroup.
+//  - Grids that fill the chip with one split (g s_lo >= R for 4-wave groups):
+//    each shape takes its best split count (best_splits) and the shape with
+//    the shorter time wins, the wide one counted kWideGain faster; idle waves
+//    of partly filled row groups show up as more row groups per split.
+//  - Smaller grids take 4-wave groups and about two rounds of work items.
+// No split is shorter than the dtype's minimum (the partial state of a split
 // costs as many bytes as ~M/2 keys of K/V, M = rows sharing it; fp32 splits
 // are compute-bound and can be shorter) or longer than the staged page list
-// allows.
-int choose_split(const d2sd_attn_args* a, int G) {
-  if (a->kv_split > 0) return a->kv_split;
+// allows. An explicit kv_split or row_group fixes that choice.
+void choose_shape(const d2sd_attn_args* a, int G, int* waves, int* split) {
+  const bool bf16 = a->dtype == D2SD_BF16;
   const int ctx = a->max_ctx_len;
-  const int min_split = a->dtype == D2SD_F32 ? kMinSplitF32 : kMinSplit;
-  if (ctx <= min_split) return ((max(ctx, 1) + 63) / 64) * 64;
-  const long long base = groups_per_split(a, G);
-  const long long resident = (long long)kNumCUs * (a->dtype == D2SD_BF16 ? 3 : 1);
+  const int min_split = bf16 ? kMinSplit : kMinSplitF32;
   const int s_lo = max(1, (ctx + kMaxSplit - 1) / kMaxSplit);
   const int s_hi = max(s_lo, ctx / min_split);
-  int splits;
-  if (base * s_lo >= resident) {
-    auto rounds_per_split = [&](int s) { return (double)((base * s + resident - 1) / resident) / s; };
-    splits = s_lo;
-    double best = rounds_per_split(s_lo);
-    for (int s = s_lo + 1; s <= min(s_hi, 4 * s_lo); ++s) {
-      const double t = rounds_per_split(s);
-      if (t < 0.97 * best) {
-        best = t;
-        splits = s;
-      }
+  const long long g4 = groups_per_split(a, G, d2sd::kBf16Waves * d2sd::kRowsPerTile);
+  const long long R4 = (long long)kNumCUs * (bf16 ? 3 : 1);
+  const long long g12 = groups_per_split(a, G, d2sd::kBf16WideWaves * d2sd::kRowsPerTile);
+  const long long R12 = kNumCUs;
+  const bool wide_ok = bf16 && a->row_group != d2sd::kBf16Waves * d2sd::kRowsPerTile;
+  const bool wide_forced = bf16 && a->row_group == d2sd::kBf16WideWaves * d2sd::kRowsPerTile;
+  int s = 0;
+  *waves = d2sd::kBf16Waves;
+  if (a->kv_split > 0) {
+    *split = a->kv_split;
+    s = max(1, (ctx + a->kv_split - 1) / a->kv_split);
+    if (wide_forced || (wide_ok && g4 * s >= R4 &&
+                        rounds_time(g12, R12, s) / kWideGain < rounds_time(g4, R4, s)))
+      *waves = d2sd::kBf16WideWaves;
+    return;
+  }
+  if (ctx <= min_split) {
+    s = 1;
+    if (wide_forced || (wide_ok && g4 >= R4 && rounds_time(g12, R12, 1) / kWideGain < rounds_time(g4, R4, 1)))
+      *waves = d2sd::kBf16WideWaves;
+  } else if (g4 * s_lo >= R4 || wide_forced) {
+    double t4 = 0.0, t12 = 0.0;
+    const int s4 = best_splits(g4, R4, s_lo, s_hi, &t4);
+    const int s12 = best_splits(g12, R12, s_lo, s_hi, &t12);
+    if (wide_forced || (wide_ok && t12 / kWideGain < t4)) {
+      *waves = d2sd::kBf16WideWaves;
+      s = s12;
+    } else {
+      s = s4;
     }
   } else {
-    splits = (int)((2 * resident + base - 1) / base);
-    splits = max(s_lo, min(splits, s_hi));
+    s = (int)((2 * R4 + g4 - 1) / g4);
+    s = max(s_lo, min(s, s_hi));
   }
-  const int per = (ctx + splits - 1) / splits;
-  return ((per + 63) / 64) * 64;
+  if (ctx <= min_split) {
+    *split = ((max(ctx, 1) + 63) / 64) * 64;
+  } else {
+    const int per = (ctx + s - 1) / s;
+    *split = ((per + 63) / 64) * 64;
+  }
 }
 
 d2sd_status make_plan(const d2sd_attn_args* a, d2sd::AttnPlan* plan) {
   plan->G = a->num_qo_heads / a->num_kv_heads;
-  plan->split = choose_split(a, plan->G);
+  choose_shape(a, plan->G, &plan->waves, &plan->split);
   const bool ctx = a->stage != D2SD_STAGE_TREE;
   plan->n_ch_max = ctx ? max(1, (a->max_ctx_len + plan->split - 1) / plan->split) : 1;
   const long long max_rows = (long long)a->max_nodes * plan->G;
-  const int rows_per_group = d2sd::group_rows(a->dtype);
+  const int rows_per_group = plan->waves * d2sd::kRowsPerTile;
   plan->n_rg_max = (int)max(1ll, (max_rows + rows_per_group - 1) / rows_per_group);
   plan->items = (long long)a->batch * a->num_kv_heads * plan->n_ch_max * plan->n_rg_max;
   if (plan->items > (1ll << 30)) return fail(D2SD_ERR_UNSUPPORTED, "too many work items (%lld)", plan->items);
@@ -417,6 +466,16 @@ d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split) {
   return ok();
 }
 
+d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows) {
+  d2sd_status s = validate_attn(args, false);
+  if (s) return s;
+  if (!rows) return fail(D2SD_ERR_INVALID_ARG, "rows is NULL");
+  d2sd::AttnPlan plan;
+  if ((s = make_plan(args, &plan))) return s;
+  *rows = plan.waves * d2sd::kRowsPerTile;
+  return ok();
+}
+
 d2sd_status d2sd_cascade_workspace_size(const d2sd_attn_args* args, size_t* bytes) {
   d2sd_status s = validate_attn(args, false);
   if (s) return s;
@@ -490,9 +549,9 @@ d2sd_status d2sd_noncascade_verify_attention(const d2sd_attn_args* args, hipStre
     return fail(D2SD_ERR_INVALID_ARG, "the non-cascade baseline computes STAGE_CASCADE only");
   if ((long long)args->batch * args->num_kv_heads * args->max_nodes > (1ll << 30))
     return fail(D2SD_ERR_UNSUPPORTED, "too many work items");
-  if (args->num_qo_heads / args->num_kv_heads > d2sd::group_rows(args->dtype))
+  if (args->num_qo_heads / args->num_kv_heads > 4 * d2sd::kRowsPerTile)
     return fail(D2SD_ERR_UNSUPPORTED, "the baseline supports at most %d query heads per KV head",
-                d2sd::group_rows(args->dtype));
+                4 * d2sd::kRowsPerTile);
   if (args->dtype == D2SD_BF16 && args->max_ctx_len > kMaxSplit)
     return fail(D2SD_ERR_UNSUPPORTED, "the baseline streams at most %d context tokens per request", kMaxSplit);
   if (args->total_nodes == 0) return ok();

@@ -439,9 +439,14 @@ __global__ __launch_bounds__(kThreads) void noncascade_attention_kernel(Params p
 }
 
 // ---------------------------------------------------------------------------
-// bf16 kernel (the hot path): workgroups of 4 waves, one 32-query column tile
-// per wave, three workgroups per CU (40 KB of LDS and 163 VGPRs each), so
-// every SIMD interleaves three independent waves. K/V tiles of 32 keys are
+// bf16 kernel (the hot path), in two workgroup shapes with the same body and
+// one 32-query column tile per wave (163 VGPRs: three waves per SIMD):
+//  - 4 waves (128 query rows), three workgroups per CU (40 KB of LDS each):
+//    every SIMD interleaves three independent waves;
+//  - 12 waves (384 query rows), one workgroup per CU: the three waves of a
+//    SIMD share one K/V ring, so a context split is copied from HBM once per
+//    384 rows instead of once per 128 (eight of the waves issue the copies).
+// The host planner takes the wide shape when its rows fill the waves as well. K/V tiles of 32 keys are
 // copied global -> LDS by the LDS DMA path (global_load_lds_dwordx4: no
 // staging registers, no VALU) into a two-stage ring: the copy of tile j+1 is
 // in flight while tile j is consumed. Both tiles keep the natural [key][dim]
@@ -454,16 +459,23 @@ __global__ __launch_bounds__(kThreads) void noncascade_attention_kernel(Params p
 // k0..k0+3 of dim d0 + i, which is the key order of the P^T slots.
 
 namespace bf {
-constexpr int WAVES = kBf16Waves;        // waves per workgroup, one 32-query tile each
-constexpr int THREADS = WAVES * kWave;
 constexpr int MAX_SPLIT_PAGES = 2048;    // page ids of one context split staged in LDS
 constexpr int KT = 32;                   // keys per tile (a 40 KB workgroup: three per CU)
 constexpr int NKB = KT / 32;             // 32-key MFMA blocks per tile
 constexpr int ROW_BYTES = kD * 2;        // 256 B per key row
 constexpr int TILE_BYTES = KT * ROW_BYTES;  // 8 KB for K (and for V)
 constexpr int BLOCKS = KT / 4;           // 1 KB (four-row) DMA blocks per K or V tile
-constexpr int WAVE_BLOCKS = BLOCKS / WAVES;   // K (and V) blocks copied by each wave
 constexpr float kRescaleLog2 = 8.0f;     // move the running max when it grows by > 2^8
+// Workgroup shape: W waves, the first COPY_WAVES of which issue the copies,
+// WAVE_BLOCKS K (and V) blocks each.
+template <int W>
+struct Shape {
+  static constexpr int WAVES = W;
+  static constexpr int THREADS = W * kWave;
+  static constexpr int COPY_WAVES = W < 8 ? W : 8;
+  static constexpr int WAVE_BLOCKS = BLOCKS / COPY_WAVES;
+  static_assert(BLOCKS % COPY_WAVES == 0, "copy blocks per wave");
+};
 }  // namespace bf
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -513,19 +525,22 @@ struct TileSrc {
   int key_end;
 };
 
-// Per-lane constants of the DMA copy: this wave copies K/V blocks
-// w, w + WAVES, ... (rows 4b .. 4b+3 of the tile, one 16-byte chunk per lane).
+// Per-lane constants of the DMA copy: copying wave w (w < CW) copies K/V
+// blocks w, w + CW, ... (rows 4b .. 4b+3 of the tile, one 16-byte chunk per lane).
+template <int CW>
 struct DmaLane {
-  int row[bf::WAVE_BLOCKS];   // tile row of the lane's chunk in each block
-  int kcol[bf::WAVE_BLOCKS];  // element offset of the logical K chunk to fetch
-  int vcol[bf::WAVE_BLOCKS];  // element offset of the logical V chunk to fetch
+  static constexpr int N = bf::BLOCKS / CW;
+  int row[N];   // tile row of the lane's chunk in each block
+  int kcol[N];  // element offset of the logical K chunk to fetch
+  int vcol[N];  // element offset of the logical V chunk to fetch
 };
 
-__device__ __forceinline__ DmaLane dma_lane(int wave, int lane) {
-  DmaLane d;
+template <int CW>
+__device__ __forceinline__ DmaLane<CW> dma_lane(int wave, int lane) {
+  DmaLane<CW> d;
 #pragma unroll
-  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
-    const int blk = wave + bf::WAVES * j;
+  for (int j = 0; j < DmaLane<CW>::N; ++j) {
+    const int blk = wave + CW * j;
     const int r = 4 * blk + (lane >> 4);
     const int p = lane & 15;          // physical chunk written by this lane
     d.row[j] = r;
@@ -538,14 +553,15 @@ __device__ __forceinline__ DmaLane dma_lane(int wave, int lane) {
 // Issue the LDS DMA of one K/V tile into a stage (sK, sV: 16 KB each).
 // Rows past the valid keys are copied from row 0 (their scores are masked,
 // so they only need to be finite).
+template <int CW>
 __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int h, int node_base,
-                                         const int* s_pid, int c0, const DmaLane& d, char* sK, char* sV) {
+                                         const int* s_pid, int c0, const DmaLane<CW>& d, char* sK, char* sV) {
   const __bf16* kc = static_cast<const __bf16*>(p.k_cache);
   const __bf16* vc = static_cast<const __bf16*>(p.v_cache);
   const int nvalid = ts.key_end - ts.key0;
   const int wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
+  for (int j = 0; j < DmaLane<CW>::N; ++j) {
     const int r = d.row[j];
     const int rs = r < nvalid ? r : 0;
     size_t rowoff;
@@ -562,7 +578,7 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
       kb = static_cast<const __bf16*>(p.k_tree);
       vb = static_cast<const __bf16*>(p.v_tree);
     }
-    const uint32_t blk_off = (uint32_t)__builtin_amdgcn_readfirstlane(wave + bf::WAVES * j) * 1024u;
+    const uint32_t blk_off = (uint32_t)__builtin_amdgcn_readfirstlane(wave + CW * j) * 1024u;
     dma16(kb + rowoff + d.kcol[j], lds_addr(sK) + blk_off);
     dma16(vb + rowoff + d.vcol[j], lds_addr(sV) + blk_off);
   }
@@ -574,17 +590,19 @@ __device__ __forceinline__ void dma_tile(const Params& p, const TileSrc& ts, int
 // staged page ids (page * hkv + h) of the wave's blocks, read beforehand by
 // ctx_tile_pages, so that the steady state can read them a step ahead.
 constexpr int kPagesPerTile = bf::KT / D2SD_PAGE_SIZE;
-__device__ __forceinline__ void ctx_tile_pages(const int* s_pid, int tile, int wave_s, int (&ph)[bf::WAVE_BLOCKS]) {
+template <int CW>
+__device__ __forceinline__ void ctx_tile_pages(const int* s_pid, int tile, int wave_s, int (&ph)[bf::BLOCKS / CW]) {
 #pragma unroll
-  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) ph[j] = s_pid[kPagesPerTile * tile + ((wave_s + bf::WAVES * j) >> 2)];
+  for (int j = 0; j < bf::BLOCKS / CW; ++j) ph[j] = s_pid[kPagesPerTile * tile + ((wave_s + CW * j) >> 2)];
 }
-__device__ __forceinline__ void dma_ctx_pages(const Params& p, const int (&ph)[bf::WAVE_BLOCKS], int wave_s,
+template <int CW>
+__device__ __forceinline__ void dma_ctx_pages(const Params& p, const int (&ph)[bf::BLOCKS / CW], int wave_s,
                                               uint32_t koff, uint32_t voff, const char* sK, const char* sV) {
   const char* kc = static_cast<const char*>(p.k_cache);
   const char* vc = static_cast<const char*>(p.v_cache);
 #pragma unroll
-  for (int j = 0; j < bf::WAVE_BLOCKS; ++j) {
-    const uint32_t blk = wave_s + bf::WAVES * j;
+  for (int j = 0; j < bf::BLOCKS / CW; ++j) {
+    const uint32_t blk = wave_s + CW * j;
     const size_t off = (size_t)(uint32_t)__builtin_amdgcn_readfirstlane(ph[j]) << 12;  // 16 rows x 256 B
     dma16s(kc + off, koff, lds_addr(sK) + blk * 1024u);
     dma16s(vc + off, voff, lds_addr(sV) + blk * 1024u);
@@ -716,9 +734,11 @@ __device__ __forceinline__ uint64_t tree_bits(const Params& p, int node_base, in
   return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
-template <bool kNode>
+template <bool kNode, int W>
 __device__ __forceinline__ void bf16_attention_body(const Params& p) {
-  constexpr int GROUP_ROWS = bf::WAVES * kRowsPerTile;
+  using S = bf::Shape<W>;
+  constexpr int CW = S::COPY_WAVES;
+  constexpr int GROUP_ROWS = S::WAVES * kRowsPerTile;
   // the two stages of the K/V ring
   __shared__ __attribute__((aligned(1024))) char sk0[bf::TILE_BYTES], sv0[bf::TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char sk1[bf::TILE_BYTES], sv1[bf::TILE_BYTES];
@@ -775,7 +795,7 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
   {
     const int npg = ceil_div(c1 - c0, D2SD_PAGE_SIZE);
     const int* pt = p.page_table + (size_t)b * p.max_pages + (c0 >> 4);
-    for (int i = threadIdx.x; i < npg; i += bf::THREADS) s_pid[i] = clampi(pt[i], 0, p.num_pages - 1) * p.hkv + h;
+    for (int i = threadIdx.x; i < npg; i += S::THREADS) s_pid[i] = clampi(pt[i], 0, p.num_pages - 1) * p.hkv + h;
   }
   bf16x8 q[8];
   load_q(p, q, valid ? static_cast<const __bf16*>(p.q) + (size_t)qrow * kD : nullptr, hf);
@@ -795,7 +815,7 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
     ts.key_end = ts.tree ? Nb : c1;
     return ts;
   };
-  const DmaLane dl = dma_lane(wave, lane);
+  const DmaLane<CW> dl = dma_lane<CW>(wave, lane);
   const ReadLane rl = read_lane(lane);
   // fast-path lane offsets: row within the page and swizzled source chunk
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
@@ -803,13 +823,14 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
   const uint32_t koff = prow * bf::ROW_BYTES + (((lane & 15) ^ prow) << 4);
   const uint32_t voff = prow * bf::ROW_BYTES + (((lane & 15) ^ ((prow & 3) << 2)) << 4);
   auto copy_tile = [&](int j, const char* sK, const char* sV) {
+    if (wave_s >= CW) return;   // wave-uniform: only the copying waves
     const TileSrc ts = src(j);
     if (!ts.tree && ts.key_end - ts.key0 >= bf::KT) {
-      int ph[bf::WAVE_BLOCKS];
-      ctx_tile_pages(s_pid, j, wave_s, ph);
-      dma_ctx_pages(p, ph, wave_s, koff, voff, sK, sV);
+      int ph[S::WAVE_BLOCKS];
+      ctx_tile_pages<CW>(s_pid, j, wave_s, ph);
+      dma_ctx_pages<CW>(p, ph, wave_s, koff, voff, sK, sV);
     } else
-      dma_tile(p, ts, h, node_base, s_pid, c0, dl, const_cast<char*>(sK), const_cast<char*>(sV));
+      dma_tile<CW>(p, ts, h, node_base, s_pid, c0, dl, const_cast<char*>(sK), const_cast<char*>(sV));
   };
 
   // prologue: tile 0 in flight
@@ -841,12 +862,14 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
   // reads the page ids of the tile it will queue next one step ahead (the
   // staged page list does not change after the prologue).
   const int n_full = c1 > c0 ? (c1 - c0) / bf::KT : 0;
-  int ph_next[bf::WAVE_BLOCKS];
-  if (n_full > 2) ctx_tile_pages(s_pid, 1, wave_s, ph_next);
+  int ph_next[S::WAVE_BLOCKS];
+  if (n_full > 2 && wave_s < CW) ctx_tile_pages<CW>(s_pid, 1, wave_s, ph_next);
   auto fast_step = [&](int jt, const char* cK, const char* cV, const char* nK, const char* nV) {
     sync_keep<0>();
-    dma_ctx_pages(p, ph_next, wave_s, koff, voff, nK, nV);    // tile jt + 1
-    if (jt + 2 < n_full) ctx_tile_pages(s_pid, jt + 2, wave_s, ph_next);
+    if (wave_s < CW) {
+      dma_ctx_pages<CW>(p, ph_next, wave_s, koff, voff, nK, nV);    // tile jt + 1
+      if (jt + 2 < n_full) ctx_tile_pages<CW>(s_pid, jt + 2, wave_s, ph_next);
+    }
     if (!active) return;
     f32x16 s[bf::NKB];
     qk_tile(cK, rl, q, s);
@@ -903,14 +926,18 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
   }
 }
 
-__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ __launch_bounds__(bf::Shape<kBf16Waves>::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void cascade_bf16_kernel(Params p) {
-  bf16_attention_body<false>(p);
+  bf16_attention_body<false, kBf16Waves>(p);
+}
+__global__ __launch_bounds__(bf::Shape<kBf16WideWaves>::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+void cascade_bf16_wide_kernel(Params p) {
+  bf16_attention_body<false, kBf16WideWaves>(p);
 }
 // The non-cascade baseline: the same body, one workgroup per (request, node, KV head).
-__global__ __launch_bounds__(bf::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ __launch_bounds__(bf::Shape<kBf16Waves>::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void noncascade_bf16_kernel(Params p) {
-  bf16_attention_body<true>(p);
+  bf16_attention_body<true, kBf16Waves>(p);
 }
 
 // Log-sum-exp reduction of the split partials of every output row (rows of
@@ -1053,8 +1080,10 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
   const Params p = make_params(a, plan, ws);
   const int grid = (int)(((plan.items + 7) / 8) * 8);
   if (ev[0]) (void)hipEventRecord(ev[0], stream);
-  if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
+  if (a.dtype == D2SD_BF16 && plan.waves == kBf16WideWaves)
+    hipLaunchKernelGGL(cascade_bf16_wide_kernel, dim3(grid), dim3(bf::Shape<kBf16WideWaves>::THREADS), 0, stream, p);
+  else if (a.dtype == D2SD_BF16)
+    hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::Shape<kBf16Waves>::THREADS), 0, stream, p);
   else
     hipLaunchKernelGGL(cascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
   if (ev[1]) (void)hipEventRecord(ev[1], stream);
@@ -1084,6 +1113,7 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
                                        hipEvent_t (&ev)[3]) {
   AttnPlan plan{};
   plan.G = a.num_qo_heads / a.num_kv_heads;
+  plan.waves = kBf16Waves;
   plan.split = 1 << 30;  // whole context in one pass
   plan.n_ch_max = 1;
   plan.n_rg_max = 1;
@@ -1093,7 +1123,7 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
   const int grid = (int)(((plan.items + 7) / 8) * 8);
   if (ev[0]) (void)hipEventRecord(ev[0], stream);
   if (a.dtype == D2SD_BF16)
-    hipLaunchKernelGGL(noncascade_bf16_kernel, dim3(grid), dim3(bf::THREADS), 0, stream, p);
+    hipLaunchKernelGGL(noncascade_bf16_kernel, dim3(grid), dim3(bf::Shape<kBf16Waves>::THREADS), 0, stream, p);
   else
     hipLaunchKernelGGL(noncascade_attention_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, p);
   if (ev[1]) (void)hipEventRecord(ev[1], stream);

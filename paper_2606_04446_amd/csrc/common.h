@@ -29,6 +29,7 @@ __device__ __forceinline__ uint32_t range_bits(int lo, int hi, int w) {
 // Resolved plan of one verify-attention call (host side).
 struct AttnPlan {
   int G;             // query heads per KV head
+  int waves;         // waves (query tiles) per workgroup: 4, or 12 for the wide bf16 shape
   int split;         // context tokens per split (multiple of 64)
   int n_ch_max;      // splits of the longest context (>= 1)
   int n_rg_max;      // row groups of the largest request (>= 1)
@@ -56,18 +57,17 @@ hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const fl
                               const float* o_b, const float* lse_b, float* o_out, float* lse_out,
                               hipStream_t stream);
 
-// Waves (one 32-query column tile each) per workgroup of the bf16 kernel.
-// Four-wave workgroups let three workgroups share a CU, so each SIMD runs
-// three independent waves that hide each other's barrier and copy waits.
+// Waves (one 32-query column tile each) per workgroup of the bf16 kernel,
+// in its two shapes. Four-wave workgroups let three workgroups share a CU,
+// so each SIMD runs three independent waves that hide each other's barrier
+// and copy waits; twelve-wave workgroups (one per CU, three waves per SIMD)
+// share one K/V ring among 384 query rows.
 constexpr int kBf16Waves = 4;
+constexpr int kBf16WideWaves = 12;
 
-// Rows (queries) per MFMA column tile, and rows per workgroup row group of
-// the cascade kernel (one tile per wave: kBf16Waves for bf16, 4 for fp32);
-// the host planner and the kernels must agree on them.
+// Rows (queries) per MFMA column tile. A work item's row group is one tile
+// per wave: 32 * plan.waves rows (fp32: always 4 waves).
 constexpr int kRowsPerTile = 32;
-__host__ __device__ constexpr int group_rows(int dtype) {
-  return (dtype == D2SD_BF16 ? kBf16Waves : 4) * kRowsPerTile;
-}
 
 // Split merge: 16 lanes per output row (8 dims each) and kMergeGroups(n)
 // groups of them per row, each folding every kMergeGroups-th split; a

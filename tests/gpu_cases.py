@@ -47,7 +47,7 @@ class Case:
                                  poison_slack=poison_slack) if tensors else None
 
     # ---- HIP path ----
-    def attention(self, stage=0, kv_split=0, out=None, lse=None, host_offsets=False):
+    def attention(self, stage=0, kv_split=0, out=None, lse=None, host_offsets=False, row_group=0):
         """host_offsets: hand the host copy of the node offsets to the planner,
         as the benchmark does (the automatic split then counts work items exactly)."""
         m = d2sd()
@@ -56,7 +56,7 @@ class Case:
             x["q"], x["k_cache"], x["v_cache"], self.d_pt, self.d_ctx, x["k_tree"], x["v_tree"], self.d_ip,
             self.tree["anc_mask"], total_nodes=self.total, max_nodes=self.max_nodes,
             max_ctx_len=int(self.layout.ctx_len.max(initial=0)), stage=stage, kv_split=kv_split, out=out,
-            lse=lse, node_indptr_host=self.node_indptr if host_offsets else None)
+            lse=lse, node_indptr_host=self.node_indptr if host_offsets else None, row_group=row_group)
 
     def resolved_split(self, kv_split=0, host_offsets=False):
         """The split length the library takes for this batch."""

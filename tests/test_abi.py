@@ -275,39 +275,62 @@ def test_node_indptr_host_validation():
     assert ws_size(_with_host_indptr(good_args(total_nodes=int(big[-1])), big))[0] == d2sd.ERR_INVALID_ARG
 
 
-def _rounds_rule(groups: int, ctx: int, min_split: int = 256, resident: int = 768) -> int:
-    """The split length the planner documents for a grid of at least one round:
-    the split count s minimising ceil(g s / R) / s, more splits only for >= 3%."""
-    s_lo = max(1, -(-ctx // 32768))
-    s_hi = max(s_lo, ctx // min_split)
-    best_s, best = s_lo, -(-groups * s_lo // resident) / s_lo
+def _best_splits(g, R, s_lo, s_hi):
+    """The split count minimising ceil(g s / R) / s, more splits only for >= 3%."""
+    best_s, best = s_lo, -(-g * s_lo // R) / s_lo
     for s in range(s_lo + 1, min(s_hi, 4 * s_lo) + 1):
-        t = -(-groups * s // resident) / s
+        t = -(-g * s // R) / s
         if t < 0.97 * best:
             best_s, best = s, t
-    per = -(-ctx // best_s)
-    return -(-per // 64) * 64
+    return best_s, best
+
+
+def _documented_plan(g4, g12, ctx, min_split=256, gain=1.08):
+    """(split, rows per workgroup) the planner documents for grids that fill
+    the chip with one split: each shape's best split count, and the shape
+    with the shorter time, the 384-row shape counted 8% faster."""
+    s_lo = max(1, -(-ctx // 32768))
+    s_hi = max(s_lo, ctx // min_split)
+    s4, t4 = _best_splits(g4, 768, s_lo, s_hi)
+    s12, t12 = _best_splits(g12, 256, s_lo, s_hi)
+    s, rows = (s12, 384) if t12 / gain < t4 else (s4, 128)
+    per = -(-ctx // s)
+    return -(-per // 64) * 64, rows
 
 
 @pytest.mark.parametrize("cfg", [4, 5])
 def test_automatic_split_counts_rounds(cfg):
-    """Large grids: the split count comes from the resident rounds of the
-    exact work-item count (node offsets given on the host)."""
+    """Large grids: split count and workgroup shape come from the resident
+    rounds of the exact work-item counts (node offsets given on the host)."""
     from paper_2606_04446_amd import workload as wl
     lay = wl.draw_layout(cfg)
     ip, W = d2sd.tree_plan(lay.spec.B, lay.K, lay.p)
     n = np.diff(ip)
     G = lay.spec.hq // lay.spec.hkv
-    groups = int((-(-(n * G) // 128)).sum()) * lay.spec.hkv
+    g4 = int((-(-(n * G) // 128)).sum()) * lay.spec.hkv
+    g12 = int((-(-(n * G) // 384)).sum()) * lay.spec.hkv
     ctx = int(lay.ctx_len.max())
     a = good_args(batch=lay.batch, num_qo_heads=lay.spec.hq, num_kv_heads=lay.spec.hkv, total_nodes=int(ip[-1]),
                   max_nodes=int(n.max()), max_ctx_len=ctx, num_pages=lay.num_pages, max_pages=lay.max_pages,
                   mask_words=W)
     _with_host_indptr(a, ip)
-    split = d2sd.cascade_kv_split(a)
-    assert split == _rounds_rule(groups, ctx)
-    # the bench workloads: 768 work items (one round) at one split; 2800 (3.65 rounds) -> 3 splits (10.9 rounds)
-    assert (groups, -(-ctx // split)) == {4: (768, 1), 5: (2800, 3)}[cfg]
+    split, rows = d2sd.cascade_kv_split(a), d2sd.cascade_row_group(a)
+    assert (split, rows) == _documented_plan(g4, g12, ctx)
+    # 32 requests: 768 four-wave groups (one round) or 256 twelve-wave groups (one round, each context
+    # read once) -> 384 rows, one split; 64 requests with 64 query heads: 2800 four-wave groups, three
+    # splits (10.9 rounds), against 12-wave groups that leave a sixth of their waves idle -> 128 rows
+    assert (g4, -(-ctx // split), rows) == {4: (768, 1, 384), 5: (2800, 3, 128)}[cfg]
+
+
+def test_row_group_is_validated_and_can_be_forced():
+    for bad in (64, 256, 512, -128):
+        a = good_args(row_group=bad)
+        assert ws_size(a)[0] == d2sd.ERR_INVALID_ARG and "row_group" in d2sd.last_error()
+    small = dict(batch=2, total_nodes=100, max_nodes=50, max_ctx_len=1000, num_pages=200, max_pages=100)
+    assert d2sd.cascade_row_group(good_args(**small)) == 128          # a small grid: four-wave groups
+    assert d2sd.cascade_row_group(good_args(row_group=384, **small)) == 384
+    assert d2sd.cascade_row_group(good_args(row_group=128)) == 128
+    assert d2sd.cascade_row_group(good_args(row_group=384, dtype=d2sd.F32, **small)) == 128   # fp32: one shape
 
 
 def test_workspace_sizing_and_too_small():

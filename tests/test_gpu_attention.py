@@ -1,7 +1,9 @@
 """GPU parity of the cascade verify attention against the float64 oracle.
 
 Tolerance (max abs over every output element, and over lse): 1e-4 for fp32
-inputs, 2e-2 for bf16 inputs, both with fp32 accumulation."""
+inputs, 2e-2 for bf16 inputs, both with fp32 accumulation. The bf16 cases run
+in both workgroup shapes (ROW_GROUPS: the automatic choice, which is 128 rows
+for these small grids, and 384 rows forced)."""
 
 import numpy as np
 import pytest
@@ -12,10 +14,12 @@ from tests.gpu_cases import TOL, Case, d2sd, max_abs
 
 pytestmark = pytest.mark.gpu
 
+ROW_GROUPS = [0, 384]
 
-def check_full(case, stage="cascade", kv_split=0, out=None, lse=None):
+
+def check_full(case, stage="cascade", kv_split=0, out=None, lse=None, row_group=0):
     code = {"cascade": 0, "prefix": 1, "tree": 2}[stage]
-    o, l = case.attention(stage=code, kv_split=kv_split)
+    o, l = case.attention(stage=code, kv_split=kv_split, row_group=row_group)
     torch.cuda.synchronize()
     o = o.double().cpu().numpy()
     l = l.cpu().numpy()
@@ -29,32 +33,36 @@ def check_full(case, stage="cascade", kv_split=0, out=None, lse=None):
     return worst
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_workload_full(cfg):
+def test_workload_full(cfg, row_group):
     case = Case(wl.draw_layout(cfg))
-    check_full(case)
+    check_full(case, row_group=row_group)
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("cfg", [1, 2])
 @pytest.mark.parametrize("stage", ["prefix", "tree"])
-def test_workload_stages(cfg, stage):
-    check_full(Case(wl.draw_layout(cfg)), stage)
+def test_workload_stages(cfg, stage, row_group):
+    check_full(Case(wl.draw_layout(cfg)), stage, row_group=row_group)
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("kv_split", [64, 128, 320, 512])
-def test_split_reduction(dtype, kv_split):
+def test_split_reduction(dtype, kv_split, row_group):
     """Many context splits with a ragged last split exercise the LSE reduction
     (four or more splits in the longest context: the four-group merge; two:
     the one-group merge)."""
     lay = wl.custom_layout(16, [[3, 7], [1], [], [2, 5, 9, 15]], [1000, 129, 64, 1], hq=8, hkv=2,
                            dtype=dtype, seed=11)
-    check_full(Case(lay), "cascade", kv_split)
-    check_full(Case(lay), "prefix", kv_split)
+    check_full(Case(lay), "cascade", kv_split, row_group=row_group)
+    check_full(Case(lay), "prefix", kv_split, row_group=row_group)
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_edge_shapes(dtype):
+def test_edge_shapes(dtype, row_group):
     # empty contexts, contexts not a multiple of the page or tile size, K = 0,
     # K = B-1, single extreme positions, mixed K in one batch
     rows = [[], list(range(1, 16)), [1], [15], [4, 8, 12], [], [2, 3]]
@@ -62,22 +70,24 @@ def test_edge_shapes(dtype):
     lay = wl.custom_layout(16, rows, ctx, hq=4, hkv=2, dtype=dtype, seed=12)
     case = Case(lay)
     for stage in ("cascade", "prefix", "tree"):
-        check_full(case, stage)
+        check_full(case, stage, row_group=row_group)
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_contexts_longer_than_one_split(dtype):
+def test_contexts_longer_than_one_split(dtype, row_group):
     """Contexts past the longest split (32768 tokens) take several splits and
     page ids past the first 2048 of a request; lengths are not multiples of
     the page or tile size. Automatic split and the longest explicit one."""
     lay = wl.custom_layout(16, [[3, 11], [1, 2, 14]], [70001, 33003], hq=8, hkv=2, dtype=dtype, seed=21)
     case = Case(lay, poison_slack=True)
-    check_full(case)
-    check_full(case, "cascade", kv_split=32768)
+    check_full(case, row_group=row_group)
+    check_full(case, "cascade", kv_split=32768, row_group=row_group)
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("seed", range(8))
-def test_random_layouts(seed):
+def test_random_layouts(seed, row_group):
     """Seeded random batches: block length, re-anchor sets, context lengths
     (page- and tile-ragged, some empty), head grouping, dtype and split
     length all drawn, then every output row against the oracle."""
@@ -91,23 +101,26 @@ def test_random_layouts(seed):
     dtype = "f32" if seed % 4 == 3 else "bf16"
     kv_split = int(rng.choice([0, 64, 256, 1024]))
     lay = wl.custom_layout(B, rows, ctx, hq=hq, hkv=hkv, dtype=dtype, seed=seed)
-    check_full(Case(lay, poison_slack=True), "cascade", kv_split)
+    check_full(Case(lay, poison_slack=True), "cascade", kv_split, row_group=row_group)
 
 
-@pytest.mark.parametrize("hq,hkv", [(8, 8), (12, 4), (64, 8), (6, 1)])
-def test_gqa_groupings(hq, hkv):
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
+@pytest.mark.parametrize("hq,hkv", [(8, 8), (12, 4), (64, 8), (6, 1), (256, 2)])
+def test_gqa_groupings(hq, hkv, row_group):
     lay = wl.custom_layout(16, [[2, 9], [5, 6, 7, 8]], [200, 77], hq=hq, hkv=hkv, dtype="bf16", seed=13)
-    check_full(Case(lay))
+    check_full(Case(lay), row_group=row_group)
 
 
-def test_poisoned_slack_is_never_read():
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
+def test_poisoned_slack_is_never_read(row_group):
     lay = wl.custom_layout(16, [[4], [1, 2]], [37, 250], hq=8, hkv=2, dtype="bf16", seed=14)
-    check_full(Case(lay, poison_slack=True))
-    check_full(Case(lay, poison_slack=True), "cascade", kv_split=64)
+    check_full(Case(lay, poison_slack=True), row_group=row_group)
+    check_full(Case(lay, poison_slack=True), "cascade", kv_split=64, row_group=row_group)
 
 
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
 @pytest.mark.parametrize("kv_split", [0, 64, 128, 192])
-def test_whole_tile_counts_around_the_steady_state(kv_split):
+def test_whole_tile_counts_around_the_steady_state(kv_split, row_group):
     """Context lengths giving 0-5 whole 32-key tiles per split, with and
     without a ragged tail, so that the steady-state loop (taken while the
     tile consumed and the tile queued are both whole context tiles) hands
@@ -117,14 +130,25 @@ def test_whole_tile_counts_around_the_steady_state(kv_split):
     p_rows = [sorted(rng.choice(np.arange(1, 16), size=int(rng.integers(0, 4)), replace=False).tolist())
               for _ in ctx]
     lay = wl.custom_layout(16, p_rows, ctx, hq=8, hkv=2, dtype="bf16", seed=16)
-    check_full(Case(lay, poison_slack=True), "cascade", kv_split=kv_split)
-    check_full(Case(lay), "prefix", kv_split=kv_split)
+    check_full(Case(lay, poison_slack=True), "cascade", kv_split=kv_split, row_group=row_group)
+    check_full(Case(lay), "prefix", kv_split=kv_split, row_group=row_group)
 
 
-def test_large_block_trees():
-    # B = 64: up to 2080 nodes, masks of 65 words, many tree tiles
+@pytest.mark.parametrize("row_group", ROW_GROUPS)
+def test_large_block_trees(row_group):
+    # B = 64: up to 2080 nodes, masks of 65 words, many tree tiles (4160 rows per
+    # request and KV head: 33 row groups of 128 or 11 of 384)
     lay = wl.custom_layout(64, [list(range(1, 64)), [10, 30]], [100, 0], hq=4, hkv=2, dtype="bf16", seed=15)
-    check_full(Case(lay))
+    check_full(Case(lay), row_group=row_group)
+
+
+@pytest.mark.parametrize("row_group", [128, 384])
+def test_forced_shapes_many_requests(row_group):
+    """40 requests with ragged contexts, both shapes forced, against the
+    oracle on every row."""
+    lay = wl.custom_layout(16, [[1 + (b % 15)] for b in range(40)], [700 + 37 * b for b in range(40)], hq=32,
+                           hkv=8, dtype="bf16", seed=17)
+    check_full(Case(lay, poison_slack=True), row_group=row_group)
 
 
 def test_merge_state_recombines_stages():
