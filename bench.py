@@ -55,6 +55,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--kv-split", type=int, default=0)
+    ap.add_argument("--row-group", type=int, default=0, choices=[0, 128, 384],
+                    help="bf16 query rows per workgroup (0: the library's choice)")
+    ap.add_argument("--packed", type=int, default=0, choices=[0, 1, 2],
+                    help="384-row workgroups over all streams' tiles: 0 the library's choice, 1 off, 2 on")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--noncascade", action="store_true",
@@ -358,9 +362,11 @@ def main():
     lse = torch.empty(x["q"].shape[:2], dtype=torch.float32, device=dev)
     a = d2sd.attn_args(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"], d_ip,
                        tree["anc_mask"], out, lse, total_nodes=total, max_nodes=max_nodes, max_ctx_len=max_ctx,
-                       kv_split=args.kv_split, node_indptr_host=node_indptr)
+                       kv_split=args.kv_split, node_indptr_host=node_indptr, row_group=args.row_group,
+                       packed=args.packed)
     ws_bytes = d2sd.cascade_workspace_size(a)
     kv_split = d2sd.cascade_kv_split(a)
+    row_group, packed = d2sd.cascade_shape(a)
     n_splits = -(-max_ctx // kv_split) if max_ctx > 0 else 1
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     acc = d2sd.accept_path(B, d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax)
@@ -369,7 +375,8 @@ def main():
         d2sd.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], d_pt, d_ctx, x["k_tree"], x["v_tree"],
                                       d_ip, tree["anc_mask"], total_nodes=total, max_nodes=max_nodes,
                                       max_ctx_len=max_ctx, stage=stage, kv_split=args.kv_split, out=o, lse=l,
-                                      workspace=ws, node_indptr_host=node_indptr)
+                                      workspace=ws, node_indptr_host=node_indptr, row_group=args.row_group,
+                                      packed=args.packed)
 
     if args.profile_stage:
         # Attention calls of one stage only (e.g. the tree-suffix tiles alone),
@@ -395,7 +402,8 @@ def main():
         splits = n_splits if stage != d2sd.STAGE_TREE else 1
         # the keys read by --record-traffic: dtype, config, requested_kv_split, roofline.splits
         print(json.dumps({"profile_stage": args.profile_stage, "dtype": spec.dtype, "calls": len(kern),
-                          "config": {"workload": spec.name, "kv_split": kv_split, "tree": args.tree},
+                          "config": {"workload": spec.name, "kv_split": kv_split, "row_group": row_group,
+                                     "packed": packed, "tree": args.tree},
                           "requested_kv_split": args.kv_split, "roofline": {"splits": splits},
                           "kernel_ms": round(k_ms, 4), "merge_ms": round(float(np.mean(merge)), 4),
                           "algorithmic_flop_per_call": flops, "tflops": round(flops / (k_ms / 1e3) / 1e12, 3)}),
@@ -546,7 +554,8 @@ def main():
         "config": {"workload": spec.name, "batch": layout.batch,
                    "ctx_len": [int(ctx.min()), int(ctx.max())], "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "block": B, "branches": spec.K, "tree_nodes": total,
-                   "page_size": spec.page_size, "kv_split": kv_split, "tree": args.tree},
+                   "page_size": spec.page_size, "kv_split": kv_split, "row_group": row_group, "packed": packed,
+                   "tree": args.tree},
         "roofline": roof,
         "roofline_note": ("mfma-bound: the workload's algorithmic flops at the bf16 dense peak take longer "
                           "than its prefix K/V bytes at the HBM peak" if roof["bound"] == "mfma" else

@@ -251,6 +251,12 @@ typedef struct d2sd_attn_args {
   int row_group;     /* bf16 query rows per workgroup: 0 = automatic, 128 (4 waves,
                         three workgroups per CU) or 384 (12 waves sharing one K/V
                         ring, one workgroup per CU); fp32 always takes 128 */
+  int packed;        /* 384-row workgroups: 0 = automatic, 1 = one stream (request,
+                        KV head, split) per workgroup, 2 = workgroups over the
+                        sequence of all streams' query tiles (several streams per
+                        workgroup, no idle waves) when node_indptr_host is given,
+                        every stream has >= 6 tiles of 32 rows, batch <= 2048 and
+                        the split is <= 16384 tokens; else as 1 */
   const void* q;
   const void* k_cache;
   const void* v_cache;
@@ -283,9 +289,11 @@ d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split);
 
 /*
  * Host. The query rows per workgroup (128 or 384) the attention call will use
- * for `args` (args->row_group if nonzero, else the automatic choice).
+ * for `args` (args->row_group if nonzero, else the automatic choice), and in
+ * *packed (nullable) 1 when the 384-row workgroups run over the sequence of
+ * all streams' tiles (args->packed), else 0.
  */
-d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows);
+d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows, int* packed);
 
 /*
  * Device. Verify attention (see d2sd_attn_args). The M = N_b * G query rows

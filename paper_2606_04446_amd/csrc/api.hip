@@ -159,6 +159,7 @@ d2sd_status validate_attn(const d2sd_attn_args* a, bool need_ws_fields) {
   if (a->kv_split < 0 || a->kv_split % 64 || a->kv_split > kMaxSplit)
     return fail(D2SD_ERR_INVALID_ARG, "kv_split %d must be 0 or a multiple of 64 in [64, %d]", a->kv_split,
                 kMaxSplit);
+  if (a->packed < 0 || a->packed > 2) return fail(D2SD_ERR_INVALID_ARG, "packed %d must be 0, 1 or 2", a->packed);
   if (a->row_group != 0 && a->row_group != d2sd::kBf16Waves * d2sd::kRowsPerTile &&
       a->row_group != d2sd::kBf16WideWaves * d2sd::kRowsPerTile)
     return fail(D2SD_ERR_INVALID_ARG, "row_group %d must be 0, %d or %d", a->row_group,
@@ -235,70 +236,135 @@ int best_splits(long long g, long long R, int s_lo, int s_hi, double* t) {
 // 8% on the 32-request, 16k-context workload.
 constexpr double kWideGain = 1.08;
 
+// Query tiles (32 rows) of one split over the batch and KV heads, for the
+// packed shape; false when it does not apply (no host node offsets, a batch
+// over kPackedMaxBatch, or a stream with fewer than kPackedMinTiles tiles).
+bool packed_tiles(const d2sd_attn_args* a, int G, long long* tiles1) {
+  if (a->dtype != D2SD_BF16 || !a->node_indptr_host || a->batch > d2sd::kPackedMaxBatch) return false;
+  long long t = 0;
+  for (int b = 0; b < a->batch; ++b) {
+    const long long rows = (long long)(a->node_indptr_host[b + 1] - a->node_indptr_host[b]) * G;
+    const long long tb = (rows + d2sd::kRowsPerTile - 1) / d2sd::kRowsPerTile;
+    if (tb < d2sd::kPackedMinTiles) return false;
+    t += tb;
+  }
+  *tiles1 = t * a->num_kv_heads;
+  return true;
+}
+
+// Relative time of the packed shape at s splits: ceil(tiles s / 12)
+// workgroups in rounds of one per CU, each 1/s of a context long.
+double packed_time(long long tiles1, int s) {
+  const long long wgs = (tiles1 * s + d2sd::kBf16WideWaves - 1) / d2sd::kBf16WideWaves;
+  return rounds_time(wgs, kNumCUs, 1) / s;
+}
+
+struct Shape {
+  int waves;
+  bool packed;
+  int splits;
+};
+
+// Packing streams costs extra reads of the streams it cuts and some control
+// work per round; it has to beat the one-stream 12-wave shape by 3%.
+constexpr double kPackMargin = 0.97;
+
 // Workgroup shape and context tokens per split. R = resident workgroups:
 // three 4-wave or one 12-wave bf16 workgroup per CU, one fp32 workgroup.
 //  - Grids that fill the chip with one split (g s_lo >= R for 4-wave groups):
 //    each shape takes its best split count (best_splits) and the shape with
-//    the shorter time wins, the wide one counted kWideGain faster; idle waves
-//    of partly filled row groups show up as more row groups per split.
+//    the shorter time wins, the 12-wave shapes counted kWideGain faster; idle
+//    waves of partly filled row groups show up as more row groups per split.
+//    The packed 12-wave shape fills every wave (workgroups over the sequence
+//    of all streams' tiles) and is counted by its tiles; it is taken only
+//    when it beats the one-stream 12-wave shape by kPackMargin.
 //  - Smaller grids take 4-wave groups and about two rounds of work items.
 // No split is shorter than the dtype's minimum (the partial state of a split
 // costs as many bytes as ~M/2 keys of K/V, M = rows sharing it; fp32 splits
 // are compute-bound and can be shorter) or longer than the staged page list
-// allows. An explicit kv_split or row_group fixes that choice.
-void choose_shape(const d2sd_attn_args* a, int G, int* waves, int* split) {
+// allows. An explicit kv_split, row_group or packed fixes that choice.
+void choose_shape(const d2sd_attn_args* a, int G, d2sd::AttnPlan* plan) {
   const bool bf16 = a->dtype == D2SD_BF16;
   const int ctx = a->max_ctx_len;
   const int min_split = bf16 ? kMinSplit : kMinSplitF32;
   const int s_lo = max(1, (ctx + kMaxSplit - 1) / kMaxSplit);
   const int s_hi = max(s_lo, ctx / min_split);
+  const int s_lo_p = max(s_lo, (ctx + d2sd::kPackedMaxSplit - 1) / d2sd::kPackedMaxSplit);
   const long long g4 = groups_per_split(a, G, d2sd::kBf16Waves * d2sd::kRowsPerTile);
   const long long R4 = (long long)kNumCUs * (bf16 ? 3 : 1);
   const long long g12 = groups_per_split(a, G, d2sd::kBf16WideWaves * d2sd::kRowsPerTile);
   const long long R12 = kNumCUs;
   const bool wide_ok = bf16 && a->row_group != d2sd::kBf16Waves * d2sd::kRowsPerTile;
   const bool wide_forced = bf16 && a->row_group == d2sd::kBf16WideWaves * d2sd::kRowsPerTile;
-  int s = 0;
-  *waves = d2sd::kBf16Waves;
+  long long tiles1 = 0;
+  const bool pk_ok = wide_ok && a->packed != 1 && packed_tiles(a, G, &tiles1) && s_hi >= s_lo_p;
+  Shape sh{d2sd::kBf16Waves, false, 1};
   if (a->kv_split > 0) {
-    *split = a->kv_split;
-    s = max(1, (ctx + a->kv_split - 1) / a->kv_split);
-    if (wide_forced || (wide_ok && g4 * s >= R4 &&
-                        rounds_time(g12, R12, s) / kWideGain < rounds_time(g4, R4, s)))
-      *waves = d2sd::kBf16WideWaves;
-    return;
-  }
-  if (ctx <= min_split) {
-    s = 1;
-    if (wide_forced || (wide_ok && g4 >= R4 && rounds_time(g12, R12, 1) / kWideGain < rounds_time(g4, R4, 1)))
-      *waves = d2sd::kBf16WideWaves;
-  } else if (g4 * s_lo >= R4 || wide_forced) {
-    double t4 = 0.0, t12 = 0.0;
+    const int s = max(1, (ctx + a->kv_split - 1) / a->kv_split);
+    sh.splits = s;
+    const double t4 = rounds_time(g4, R4, s);
+    const double t12 = rounds_time(g12, R12, s) / kWideGain;
+    const bool pk_here = pk_ok && a->kv_split <= d2sd::kPackedMaxSplit;
+    const double tp = pk_here ? packed_time(tiles1, s) / kWideGain : 1e30;
+    const bool large = g4 * s >= R4;
+    if (pk_here && (a->packed == 2 || ((wide_forced || large) && tp < kPackMargin * t12 && (wide_forced || tp < t4)))) {
+      sh.waves = d2sd::kBf16WideWaves;
+      sh.packed = true;
+    } else if (wide_forced || (wide_ok && large && t12 < t4)) {
+      sh.waves = d2sd::kBf16WideWaves;
+    }
+  } else if (g4 * s_lo >= R4 || wide_forced || (pk_ok && a->packed == 2)) {
+    double t4 = 0.0, t12 = 0.0, tp = 1e30;
     const int s4 = best_splits(g4, R4, s_lo, s_hi, &t4);
     const int s12 = best_splits(g12, R12, s_lo, s_hi, &t12);
-    if (wide_forced || (wide_ok && t12 / kWideGain < t4)) {
-      *waves = d2sd::kBf16WideWaves;
-      s = s12;
-    } else {
-      s = s4;
+    t12 /= kWideGain;
+    int sp = s_lo_p;
+    if (pk_ok) {
+      tp = packed_time(tiles1, s_lo_p);
+      for (int s = s_lo_p + 1; s <= min(s_hi, 4 * s_lo_p); ++s) {
+        const double ts = packed_time(tiles1, s);
+        if (ts < 0.97 * tp) {
+          tp = ts;
+          sp = s;
+        }
+      }
+      tp /= kWideGain;
     }
-  } else {
-    s = (int)((2 * R4 + g4 - 1) / g4);
-    s = max(s_lo, min(s, s_hi));
+    if (pk_ok && (a->packed == 2 || (tp < kPackMargin * t12 && (wide_forced || tp < t4)))) {
+      sh = Shape{d2sd::kBf16WideWaves, true, sp};
+    } else if (wide_forced || (wide_ok && t12 < t4)) {
+      sh = Shape{d2sd::kBf16WideWaves, false, s12};
+    } else {
+      sh = Shape{d2sd::kBf16Waves, false, s4};
+    }
+  } else if (ctx > min_split) {
+    const int s = (int)((2 * R4 + g4 - 1) / g4);
+    sh.splits = max(s_lo, min(s, s_hi));
   }
-  if (ctx <= min_split) {
-    *split = ((max(ctx, 1) + 63) / 64) * 64;
+  plan->waves = sh.waves;
+  plan->packed = sh.packed;
+  plan->tiles = 0;   // the packed shape's tile count is set by make_plan from the resolved split count
+  if (a->kv_split > 0) {
+    plan->split = a->kv_split;
+  } else if (ctx <= min_split) {
+    plan->split = ((max(ctx, 1) + 63) / 64) * 64;
   } else {
-    const int per = (ctx + s - 1) / s;
-    *split = ((per + 63) / 64) * 64;
+    const int per = (ctx + sh.splits - 1) / sh.splits;
+    plan->split = ((per + 63) / 64) * 64;
   }
 }
 
 d2sd_status make_plan(const d2sd_attn_args* a, d2sd::AttnPlan* plan) {
   plan->G = a->num_qo_heads / a->num_kv_heads;
-  choose_shape(a, plan->G, &plan->waves, &plan->split);
+  choose_shape(a, plan->G, plan);
   const bool ctx = a->stage != D2SD_STAGE_TREE;
   plan->n_ch_max = ctx ? max(1, (a->max_ctx_len + plan->split - 1) / plan->split) : 1;
+  if (plan->packed) {
+    long long tiles1 = 0;
+    packed_tiles(a, plan->G, &tiles1);
+    plan->tiles = tiles1 * plan->n_ch_max;
+    if (plan->tiles > (1ll << 30)) return fail(D2SD_ERR_UNSUPPORTED, "too many query tiles (%lld)", plan->tiles);
+  }
   const long long max_rows = (long long)a->max_nodes * plan->G;
   const int rows_per_group = plan->waves * d2sd::kRowsPerTile;
   plan->n_rg_max = (int)max(1ll, (max_rows + rows_per_group - 1) / rows_per_group);
@@ -466,13 +532,14 @@ d2sd_status d2sd_cascade_kv_split(const d2sd_attn_args* args, int* kv_split) {
   return ok();
 }
 
-d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows) {
+d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows, int* packed) {
   d2sd_status s = validate_attn(args, false);
   if (s) return s;
   if (!rows) return fail(D2SD_ERR_INVALID_ARG, "rows is NULL");
   d2sd::AttnPlan plan;
   if ((s = make_plan(args, &plan))) return s;
   *rows = plan.waves * d2sd::kRowsPerTile;
+  if (packed) *packed = plan.packed ? 1 : 0;
   return ok();
 }
 

@@ -926,6 +926,374 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Packed twelve-wave bf16 kernel. The query tiles of all streams (request b,
+// KV head h, context split ch: T_b = ceil(N_b G / 32) tiles of 32 rows each,
+// n_ch_max splits per request, the splits a request does not need are empty)
+// form one sequence in (b, h, ch, tile) order; workgroup i takes tiles
+// 12 i .. 12 i + 11, one per wave. Consecutive waves on the same stream form
+// a segment that shares one K/V ring, so no wave is idle for lack of rows
+// and a stream is read by the one to three workgroups that hold its tiles
+// (neighbours in the dispatch order, on one XCD). The host takes this shape
+// only when every stream has at least pk::MIN_TILES tiles, so that a
+// workgroup holds at most pk::SEGS segments. All twelve waves share the
+// copies: segment s's tile is eight 1 KB K/V block pairs, pair 8 s + j goes
+// to wave (8 s + j) mod 12.
+namespace pk {
+constexpr int WAVES = 12;
+constexpr int THREADS = WAVES * kWave;
+constexpr int SEGS = 3;
+constexpr int MIN_TILES = kPackedMinTiles;            // 12 consecutive tiles span <= 3 streams
+constexpr int MAX_SPLIT_PAGES = kPackedMaxSplit / D2SD_PAGE_SIZE;
+constexpr int MAX_BATCH = kPackedMaxBatch;
+static_assert(WAVES / MIN_TILES + 1 <= SEGS, "segments per workgroup");
+constexpr int SEG_BYTES = 4 * bf::TILE_BYTES;   // two stages x (K, V)
+constexpr int PAIRS = 2;                // block pairs per wave and round: waves w and w + 12 of 24
+}  // namespace pk
+
+struct PackedSeg {
+  int b, h, ch, node_base, Nb, c0, c1, n_ctx_tiles, n_tiles, n_full, n_ch_b;
+};
+
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Tiles of request b over all its streams.
+__device__ __forceinline__ int request_tiles(const Params& p, int b) {
+  const int nb0 = clampi(p.node_indptr[b], 0, p.total_nodes);
+  const int Nb = clampi(p.node_indptr[b + 1] - nb0, 0, min(p.max_nodes, p.total_nodes - nb0));
+  return ceil_div(Nb * p.G, kRowsPerTile) * p.hkv * p.n_ch_max;
+}
+
+__device__ void bf16_packed_body(const Params& p) {
+  __shared__ __attribute__((aligned(1024))) char ring[pk::SEGS * pk::SEG_BYTES];
+  __shared__ __attribute__((aligned(16))) int s_pid[pk::SEGS][pk::MAX_SPLIT_PAGES];
+  __shared__ int s_pref[pk::MAX_BATCH + 1];
+  __shared__ int s_wsum[pk::WAVES];
+  __shared__ int s_gs[pk::WAVES];
+  __shared__ PackedSeg s_seg[pk::SEGS];
+
+  const int per_xcd = gridDim.x / 8;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int hf = lane >> 5;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const int batch = min(p.batch, pk::MAX_BATCH);
+
+  // ---- tiles before each request (block scan; up to 3 requests per thread) ----
+  {
+    constexpr int PER = (pk::MAX_BATCH + pk::THREADS - 1) / pk::THREADS;
+    int loc[PER];
+    int sum = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int b = tid * PER + k;
+      loc[k] = sum;
+      sum += b < batch ? request_tiles(p, b) : 0;
+    }
+    const int incl = wave_incl_scan(sum, lane);
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int off = 0;
+    for (int w = 0; w < wave; ++w) off += s_wsum[w];
+    const int excl = off + incl - sum;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int b = tid * PER + k;
+      if (b < batch) s_pref[b] = excl + loc[k];
+    }
+    if (tid == 0) {
+      int tot = 0;
+      for (int w = 0; w < pk::WAVES; ++w) tot += s_wsum[w];
+      s_pref[batch] = tot;
+    }
+    __syncthreads();
+  }
+
+  // ---- this wave's tile: stream (b, h, ch) and tile index ti within it ----
+  const int t = item * pk::WAVES + wave_s;
+  int gs = -1, ti = 0, wb = 0;
+  if (t < s_pref[batch]) {
+    int lo = 0, hi = batch;                 // largest b with s_pref[b] <= t
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_pref[mid] <= t) lo = mid; else hi = mid;
+    }
+    wb = lo;
+    const int per_stream = (s_pref[wb + 1] - s_pref[wb]) / (p.hkv * p.n_ch_max);   // T_b
+    const int local = t - s_pref[wb];
+    const int sidx = per_stream > 0 ? local / per_stream : 0;
+    ti = per_stream > 0 ? local - sidx * per_stream : 0;
+    gs = wb * p.hkv * p.n_ch_max + sidx;    // (b, h, ch) in sequence order
+  }
+  if (lane == 0) s_gs[wave_s] = gs;
+  __syncthreads();
+  // segment of this wave: count of stream starts among waves 0..wave
+  int seg = -1, nseg = 0;
+  for (int w = 0; w < pk::WAVES; ++w) {
+    const bool start = s_gs[w] >= 0 && (w == 0 || s_gs[w] != s_gs[w - 1]);
+    nseg += start;
+    if (w == wave_s) seg = s_gs[w] >= 0 ? nseg - 1 : -1;
+  }
+  nseg = min(nseg, pk::SEGS);
+  if (seg >= pk::SEGS) seg = -1;            // not reached when the host's size rule holds
+  const bool seg_leader = seg >= 0 && (wave_s == 0 || s_gs[wave_s - 1] != gs);
+  if (seg_leader && lane == 0) {
+    PackedSeg g;
+    const int sidx = gs - wb * p.hkv * p.n_ch_max;
+    g.b = wb;
+    g.h = sidx / p.n_ch_max;
+    g.ch = sidx - g.h * p.n_ch_max;
+    g.node_base = clampi(p.node_indptr[wb], 0, p.total_nodes);
+    g.Nb = clampi(p.node_indptr[wb + 1] - g.node_base, 0, min(p.max_nodes, p.total_nodes - g.node_base));
+    const int Cb = clampi(p.ctx_len[wb], 0, p.max_ctx);
+    const bool use_ctx = p.stage != D2SD_STAGE_TREE;
+    const bool use_tree = p.stage != D2SD_STAGE_PREFIX;
+    g.n_ch_b = use_ctx ? max(1, ceil_div(Cb, p.split)) : 1;
+    g.c0 = use_ctx ? g.ch * p.split : 0;
+    g.c1 = use_ctx ? min(Cb, g.c0 + p.split) : 0;
+    if (g.ch >= g.n_ch_b) g.c1 = g.c0;      // an empty stream
+    g.n_ctx_tiles = g.c1 > g.c0 ? ceil_div(g.c1 - g.c0, bf::KT) : 0;
+    const int n_tree = (use_tree && g.ch == 0) ? ceil_div(g.Nb, bf::KT) : 0;
+    g.n_tiles = g.ch < g.n_ch_b ? g.n_ctx_tiles + n_tree : 0;
+    g.n_full = g.c1 > g.c0 ? (g.c1 - g.c0) / bf::KT : 0;
+    s_seg[seg] = g;
+  }
+  __syncthreads();
+
+  // ---- page ids of every segment's split ----
+  for (int sg = 0; sg < nseg; ++sg) {
+    const PackedSeg& g = s_seg[sg];
+    const int npg = min(ceil_div(g.c1 - g.c0, D2SD_PAGE_SIZE), pk::MAX_SPLIT_PAGES);
+    const int* pt = p.page_table + (size_t)g.b * p.max_pages + (g.c0 >> 4);
+    for (int i = tid; i < npg; i += pk::THREADS) s_pid[sg][i] = clampi(pt[i], 0, p.num_pages - 1) * p.hkv + g.h;
+  }
+
+  // ---- this wave's rows ----
+  auto uni = [](int x) { return __builtin_amdgcn_readfirstlane(x); };
+  PackedSeg my{};
+  if (seg >= 0) {
+    const PackedSeg g = s_seg[seg];
+    my.b = uni(g.b); my.h = uni(g.h); my.ch = uni(g.ch); my.node_base = uni(g.node_base); my.Nb = uni(g.Nb);
+    my.c0 = uni(g.c0); my.c1 = uni(g.c1); my.n_ctx_tiles = uni(g.n_ctx_tiles); my.n_tiles = uni(g.n_tiles);
+    my.n_full = uni(g.n_full); my.n_ch_b = uni(g.n_ch_b);
+  }
+  const int Mb = my.Nb * p.G;
+  const int r_lo = ti * kRowsPerTile;
+  // a wave of an existing stream writes its rows even with no tile to
+  // attend to (an empty context in the prefix stage: O = 0, lse = -inf)
+  const bool active = seg >= 0 && my.ch < my.n_ch_b && r_lo < Mb;
+  const int r = r_lo + (lane & 31);
+  const bool valid = active && r < Mb;
+  const int qnode = valid ? r / p.G : 0;
+  const int qrow = valid ? (my.node_base + qnode) * p.hq + my.h * p.G + r % p.G : -1;
+  bf16x8 q[8];
+  load_q(p, q, valid ? static_cast<const __bf16*>(p.q) + (size_t)qrow * kD : nullptr, hf);
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.0f;
+  wait_vmem();          // every global load retired before the first (untracked) copy
+  __syncthreads();
+
+  int n_rounds = 0, n_fast = 1 << 30;
+  for (int sg = 0; sg < nseg; ++sg) {
+    n_rounds = max(n_rounds, s_seg[sg].n_tiles);
+    if (s_seg[sg].n_tiles > 0) n_fast = min(n_fast, s_seg[sg].n_full - 1);
+  }
+  n_rounds = uni(n_rounds);
+  n_fast = uni(max(0, min(n_fast, n_rounds)));
+
+  // LDS read offsets within this wave's segment ring
+  ReadLane rl = read_lane(lane);
+  {
+    const int so = max(seg, 0) * pk::SEG_BYTES;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) rl.k[i] += so;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rl.v[i] += so;
+  }
+  // Copy pairs of this wave: pair pr = wave + 12 jj (jj < PAIRS) when pr < 8 nseg;
+  // pair pr is segment pr / 8, block pr % 8 (tile rows 4 blk .. 4 blk + 3), and
+  // blk % 4 = wave % 4 for both pairs, so the fast-path lane offsets are per wave.
+  const int prow = 4 * (wave_s & 3) + (lane >> 4);
+  const uint32_t koff = prow * bf::ROW_BYTES + (((lane & 15) ^ prow) << 4);
+  const uint32_t voff = prow * bf::ROW_BYTES + (((lane & 15) ^ ((prow & 3) << 2)) << 4);
+  const char* kc = static_cast<const char*>(p.k_cache);
+  const char* vc = static_cast<const char*>(p.v_cache);
+  const uint32_t ring_lds = lds_addr(ring);
+  int pr_sg[pk::PAIRS], pr_blk[pk::PAIRS], pr_tiles[pk::PAIRS];
+#pragma unroll
+  for (int jj = 0; jj < pk::PAIRS; ++jj) {
+    const int pr = wave_s + pk::WAVES * jj;
+    pr_sg[jj] = pr >> 3;
+    pr_blk[jj] = pr & 7;
+    pr_tiles[jj] = pr < 8 * nseg ? uni(s_seg[pr >> 3].n_tiles) : 0;   // 0: no such pair
+  }
+  // page ids of the fast copies of tile j (read one round ahead)
+  auto dst_of = [&](int jj, int stage) {
+    return ring_lds + pr_sg[jj] * pk::SEG_BYTES + stage * (2 * bf::TILE_BYTES) + pr_blk[jj] * 1024u;
+  };
+  // copy of tile j of the pairs' segments, any tile kind
+  auto copy_any = [&](int j, int stage) {
+#pragma unroll
+    for (int jj = 0; jj < pk::PAIRS; ++jj) {
+      if (j >= pr_tiles[jj]) continue;
+      const PackedSeg& g = s_seg[pr_sg[jj]];
+      const uint32_t dst = dst_of(jj, stage);
+      const int n_ctx = uni(g.n_ctx_tiles);
+      const bool tree = j >= n_ctx;
+      const int c0 = uni(g.c0);
+      const int key0 = tree ? (j - n_ctx) * bf::KT : c0 + j * bf::KT;
+      const int nvalid = (tree ? uni(g.Nb) : uni(g.c1)) - key0;
+      const int rr = 4 * pr_blk[jj] + (lane >> 4);
+      const int rs = rr < nvalid ? rr : 0;
+      const int pc = lane & 15;
+      size_t rowoff;
+      const __bf16* kb;
+      const __bf16* vb;
+      if (!tree) {
+        const int key = key0 + rs;
+        rowoff = ((size_t)s_pid[pr_sg[jj]][min((key - c0) >> 4, pk::MAX_SPLIT_PAGES - 1)] * D2SD_PAGE_SIZE +
+                  (key & 15)) * kD;
+        kb = static_cast<const __bf16*>(p.k_cache);
+        vb = static_cast<const __bf16*>(p.v_cache);
+      } else {
+        rowoff = ((size_t)(uni(g.node_base) + key0 + rs) * p.hkv + uni(g.h)) * kD;
+        kb = static_cast<const __bf16*>(p.k_tree);
+        vb = static_cast<const __bf16*>(p.v_tree);
+      }
+      dma16(kb + rowoff + (pc ^ (rr & 15)) * 8, dst);
+      dma16(vb + rowoff + (pc ^ ((rr & 3) << 2)) * 8, dst + bf::TILE_BYTES);
+    }
+  };
+  const char* ringc = ring;
+  auto compute = [&](int j, int stage, bool fast) {
+    if (!active || j >= my.n_tiles) return;
+    const char* sK = ringc + stage * (2 * bf::TILE_BYTES);
+    const char* sV = sK + bf::TILE_BYTES;
+    f32x16 sc[bf::NKB];
+    qk_tile(sK, rl, q, sc);
+    if (!fast) {
+      const bool tree = j >= my.n_ctx_tiles;
+      const int key0 = tree ? (j - my.n_ctx_tiles) * bf::KT : my.c0 + j * bf::KT;
+      const int nvalid = (tree ? my.Nb : my.c1) - key0;
+      if (tree || nvalid < bf::KT) {
+        const uint64_t vis = tree ? tree_bits(p, my.node_base, qnode, key0) : ~0ull;
+        mask_tile(sc, nvalid, vis, hf);
+      }
+    }
+    bf16x8 pf[2 * bf::NKB];
+    softmax_tile(sc, m_run, l_run, o, pf, p.c2);
+    pv_tile(sV, rl, pf, o);
+  };
+
+  // prologue: tile 0 of every segment in flight
+  if (n_rounds > 0) copy_any(0, 0);
+  // Steady state: rounds j < n_fast consume, and queue, whole context tiles
+  // of every live segment (n_fast <= n_full - 1 <= n_tiles - 1), so a round
+  // needs no tile checks and no masks; the page ids of the copy after next
+  // are read a round ahead.
+  bool pr_on[pk::PAIRS];
+#pragma unroll
+  for (int jj = 0; jj < pk::PAIRS; ++jj) pr_on[jj] = pr_tiles[jj] > 0;
+  const bool computes = active && my.n_tiles > 0;
+  auto steady_copy = [&](int jt, int stage, const int (&ph)[pk::PAIRS]) {
+#pragma unroll
+    for (int jj = 0; jj < pk::PAIRS; ++jj) {
+      if (!pr_on[jj]) continue;
+      const size_t off = (size_t)(uint32_t)uni(ph[jj]) << 12;    // 16 rows x 256 B
+      const uint32_t dst = dst_of(jj, stage);
+      dma16s(kc + off, koff, dst);
+      dma16s(vc + off, voff, dst + bf::TILE_BYTES);
+    }
+  };
+  auto steady_pages = [&](int jt, int (&ph)[pk::PAIRS]) {
+#pragma unroll
+    for (int jj = 0; jj < pk::PAIRS; ++jj)
+      if (pr_on[jj]) ph[jj] = s_pid[pr_sg[jj]][min(2 * jt + (pr_blk[jj] >> 2), pk::MAX_SPLIT_PAGES - 1)];
+  };
+  auto steady_compute = [&](int stage) {
+    if (!computes) return;
+    const char* sK = ringc + stage * (2 * bf::TILE_BYTES);
+    f32x16 sc[bf::NKB];
+    qk_tile(sK, rl, q, sc);
+    bf16x8 pf[2 * bf::NKB];
+    softmax_tile(sc, m_run, l_run, o, pf, p.c2);
+    pv_tile(sK + bf::TILE_BYTES, rl, pf, o);
+  };
+  int ph_next[pk::PAIRS] = {0, 0};
+  if (n_fast > 1) steady_pages(1, ph_next);
+  int j = 0;
+  for (; j + 1 < n_fast; j += 2) {
+    sync_keep<0>();
+    steady_copy(j + 1, 1, ph_next);      // j + 1 < n_fast
+    steady_pages(j + 2, ph_next);
+    steady_compute(0);
+    sync_keep<0>();
+    steady_copy(j + 2, 0, ph_next);      // j + 2 <= n_fast: still a whole context tile of every live segment
+    steady_pages(j + 3, ph_next);
+    steady_compute(1);
+  }
+  // the rest: partial and tree tiles (stage j % 2)
+  for (; j < n_rounds; ++j) {
+    sync_keep<0>();
+    if (j + 1 < n_rounds) copy_any(j + 1, (j + 1) & 1);
+    compute(j, j & 1, j < n_fast);
+  }
+
+  // ---- epilogue: finalise (single split) or write the split partial ----
+  if (!active) return;
+  const float l_all = l_run + __shfl_xor(l_run, 32);
+  if (!valid) return;
+  const size_t row = (size_t)qrow;
+  if (my.n_ch_b == 1) {
+    const float inv = l_all > 0.0f ? 1.0f / l_all : 0.0f;
+    __bf16* dst = static_cast<__bf16*>(p.out) + row * kD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        float v[4];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr] * inv;
+        store_out<__bf16>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+      }
+    }
+    if (p.lse && hf == 0) p.lse[row] = l_all > 0.0f ? (m_run * p.c2 + __log2f(l_all)) * kLn2 : -INFINITY;
+  } else {
+    const size_t prow2 = (size_t)my.ch * ((size_t)p.total_nodes * p.hq) + row;
+    float* dst = p.ws_o + prow2 * kD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        float v[4];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr];
+        store_out<float>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+      }
+    }
+    if (hf == 0) {
+      p.ws_m[prow2] = l_all > 0.0f ? m_run * p.c2 : -INFINITY;
+      p.ws_l[prow2] = l_all;
+    }
+  }
+}
+
+__global__ __launch_bounds__(pk::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+void cascade_bf16_packed_kernel(Params p) {
+  bf16_packed_body(p);
+}
+
 __global__ __launch_bounds__(bf::Shape<kBf16Waves>::THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void cascade_bf16_kernel(Params p) {
   bf16_attention_body<false, kBf16Waves>(p);
@@ -1080,7 +1448,11 @@ hipError_t launch_cascade_attention(const d2sd_attn_args& a, const AttnPlan& pla
   const Params p = make_params(a, plan, ws);
   const int grid = (int)(((plan.items + 7) / 8) * 8);
   if (ev[0]) (void)hipEventRecord(ev[0], stream);
-  if (a.dtype == D2SD_BF16 && plan.waves == kBf16WideWaves)
+  if (a.dtype == D2SD_BF16 && plan.packed) {
+    const long long wgs = (plan.tiles + pk::WAVES - 1) / pk::WAVES;
+    const int pgrid = (int)(((wgs + 7) / 8) * 8);
+    hipLaunchKernelGGL(cascade_bf16_packed_kernel, dim3(pgrid), dim3(pk::THREADS), 0, stream, p);
+  } else if (a.dtype == D2SD_BF16 && plan.waves == kBf16WideWaves)
     hipLaunchKernelGGL(cascade_bf16_wide_kernel, dim3(grid), dim3(bf::Shape<kBf16WideWaves>::THREADS), 0, stream, p);
   else if (a.dtype == D2SD_BF16)
     hipLaunchKernelGGL(cascade_bf16_kernel, dim3(grid), dim3(bf::Shape<kBf16Waves>::THREADS), 0, stream, p);
@@ -1114,6 +1486,8 @@ hipError_t launch_noncascade_attention(const d2sd_attn_args& a, float scale, hip
   AttnPlan plan{};
   plan.G = a.num_qo_heads / a.num_kv_heads;
   plan.waves = kBf16Waves;
+  plan.packed = false;
+  plan.tiles = 0;
   plan.split = 1 << 30;  // whole context in one pass
   plan.n_ch_max = 1;
   plan.n_rg_max = 1;

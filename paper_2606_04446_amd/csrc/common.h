@@ -29,7 +29,9 @@ __device__ __forceinline__ uint32_t range_bits(int lo, int hi, int w) {
 // Resolved plan of one verify-attention call (host side).
 struct AttnPlan {
   int G;             // query heads per KV head
-  int waves;         // waves (query tiles) per workgroup: 4, or 12 for the wide bf16 shape
+  int waves;         // waves (query tiles) per workgroup: 4, or 12 for the wide bf16 shapes
+  bool packed;       // 12 waves over the global tile sequence (several streams per workgroup)
+  long long tiles;   // packed: query tiles of all streams (the grid holds ceil(tiles / 12) workgroups)
   int split;         // context tokens per split (multiple of 64)
   int n_ch_max;      // splits of the longest context (>= 1)
   int n_rg_max;      // row groups of the largest request (>= 1)
@@ -64,6 +66,13 @@ hipError_t launch_merge_state(int rows, int head_dim, const float* o_a, const fl
 // share one K/V ring among 384 query rows.
 constexpr int kBf16Waves = 4;
 constexpr int kBf16WideWaves = 12;
+
+// The packed twelve-wave kernel: at least kPackedMinTiles query tiles per
+// stream (so that 12 consecutive tiles span at most three streams), at most
+// kPackedMaxBatch requests and kPackedMaxSplit context tokens per split.
+constexpr int kPackedMinTiles = 6;
+constexpr int kPackedMaxBatch = 2048;
+constexpr int kPackedMaxSplit = 16384;
 
 // Rows (queries) per MFMA column tile. A work item's row group is one tile
 // per wave: 32 * plan.waves rows (fp32: always 4 waves).

@@ -52,6 +52,7 @@ class AttnArgs(ctypes.Structure):
         ("page_size", _c_int), ("dtype", _c_int), ("stage", _c_int), ("sm_scale", ctypes.c_float),
         ("total_nodes", _c_int), ("max_nodes", _c_int), ("max_ctx_len", _c_int), ("num_pages", _c_int),
         ("max_pages", _c_int), ("mask_words", _c_int), ("kv_split", _c_int), ("row_group", _c_int),
+        ("packed", _c_int),
         ("q", _c_ptr), ("k_cache", _c_ptr), ("v_cache", _c_ptr), ("page_table", _c_ptr),
         ("ctx_len", _c_ptr), ("k_tree", _c_ptr), ("v_tree", _c_ptr), ("node_indptr", _c_ptr),
         ("anc_mask", _c_ptr), ("out", _c_ptr), ("lse", _c_ptr), ("node_indptr_host", _c_ptr),
@@ -84,7 +85,7 @@ _commit = _sig("d2sd_commit_accepted_kv", _c_int, _c_int, _c_int, _c_int, _c_int
                _c_int, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr)
 _ws_size = _sig("d2sd_cascade_workspace_size", _c_int, ctypes.POINTER(AttnArgs), ctypes.POINTER(_c_size))
 _kv_split = _sig("d2sd_cascade_kv_split", _c_int, ctypes.POINTER(AttnArgs), _c_int_p)
-_row_group = _sig("d2sd_cascade_row_group", _c_int, ctypes.POINTER(AttnArgs), _c_int_p)
+_row_group = _sig("d2sd_cascade_row_group", _c_int, ctypes.POINTER(AttnArgs), _c_int_p, _c_int_p)
 _cascade = _sig("d2sd_cascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr, _c_size, _c_ptr)
 _noncascade = _sig("d2sd_noncascade_verify_attention", _c_int, ctypes.POINTER(AttnArgs), _c_ptr)
 _cascade_noalloc = _sig("d2sd_cascade_verify_attention_noalloc", _c_int, ctypes.POINTER(AttnArgs), _c_ptr)
@@ -266,7 +267,8 @@ def commit_accepted_kv(B: int, node_indptr, total_nodes: int, path_nodes, accept
 
 def attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse, *,
               total_nodes: int, max_nodes: int, max_ctx_len: int, stage: int = STAGE_CASCADE,
-              sm_scale: float = 0.0, kv_split: int = 0, node_indptr_host=None, row_group: int = 0) -> AttnArgs:
+              sm_scale: float = 0.0, kv_split: int = 0, node_indptr_host=None, row_group: int = 0,
+              packed: int = 0) -> AttnArgs:
     """Fill a d2sd_attn_args from tensors (shapes as documented in the header).
     node_indptr_host: optional host copy of node_indptr (the automatic split
     then counts the work items exactly)."""
@@ -293,6 +295,7 @@ def attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_ind
     a.mask_words = anc_mask.shape[1] if anc_mask is not None else 0
     a.kv_split = kv_split
     a.row_group = row_group
+    a.packed = packed
     a.q = _dev(q, "q", dt)
     a.k_cache = _dev(k_cache, "k_cache", dt)
     a.v_cache = _dev(v_cache, "v_cache", dt)
@@ -320,9 +323,16 @@ def cascade_workspace_size(args: AttnArgs) -> int:
 
 
 def cascade_row_group(args: AttnArgs) -> int:
+    """Query rows per workgroup (128 or 384) of the call's plan."""
+    return cascade_shape(args)[0]
+
+
+def cascade_shape(args: AttnArgs) -> tuple:
+    """(rows per workgroup, packed) of the call's plan."""
     n = ctypes.c_int(0)
-    _check(_row_group(ctypes.byref(args), ctypes.byref(n)), "d2sd_cascade_row_group")
-    return n.value
+    pk = ctypes.c_int(0)
+    _check(_row_group(ctypes.byref(args), ctypes.byref(n), ctypes.byref(pk)), "d2sd_cascade_row_group")
+    return n.value, bool(pk.value)
 
 
 def cascade_kv_split(args: AttnArgs) -> int:
@@ -334,7 +344,8 @@ def cascade_kv_split(args: AttnArgs) -> int:
 def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask,
                              *, total_nodes: int, max_nodes: int, max_ctx_len: int, stage: int = STAGE_CASCADE,
                              sm_scale: float = 0.0, kv_split: int = 0, out=None, lse=None, workspace=None,
-                             want_lse: bool = True, node_indptr_host=None, row_group: int = 0, stream=None):
+                             want_lse: bool = True, node_indptr_host=None, row_group: int = 0, packed: int = 0,
+                             stream=None):
     """Verify attention; returns (out, lse). The workspace is allocated when not given."""
     import torch
     if out is None:
@@ -343,7 +354,8 @@ def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v
         lse = torch.empty(q.shape[:2], dtype=torch.float32, device=q.device)
     a = attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse,
                   total_nodes=total_nodes, max_nodes=max_nodes, max_ctx_len=max_ctx_len, stage=stage,
-                  sm_scale=sm_scale, kv_split=kv_split, node_indptr_host=node_indptr_host, row_group=row_group)
+                  sm_scale=sm_scale, kv_split=kv_split, node_indptr_host=node_indptr_host, row_group=row_group,
+                  packed=packed)
     need = cascade_workspace_size(a)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
@@ -356,13 +368,15 @@ def cascade_verify_attention(q, k_cache, v_cache, page_table, ctx_len, k_tree, v
 def cascade_verify_attention_noalloc(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr,
                                      anc_mask, *, total_nodes: int, max_nodes: int, max_ctx_len: int,
                                      stage: int = STAGE_CASCADE, sm_scale: float = 0.0, kv_split: int = 0, out,
-                                     lse=None, node_indptr_host=None, row_group: int = 0, stream=None):
+                                     lse=None, node_indptr_host=None, row_group: int = 0, packed: int = 0,
+                                     stream=None):
     """Verify attention through the allocation-free entry point: the caller
     passes the outputs, the split partial states use the library's static
     device scratch. Returns (out, lse)."""
     a = attn_args(q, k_cache, v_cache, page_table, ctx_len, k_tree, v_tree, node_indptr, anc_mask, out, lse,
                   total_nodes=total_nodes, max_nodes=max_nodes, max_ctx_len=max_ctx_len, stage=stage,
-                  sm_scale=sm_scale, kv_split=kv_split, node_indptr_host=node_indptr_host, row_group=row_group)
+                  sm_scale=sm_scale, kv_split=kv_split, node_indptr_host=node_indptr_host, row_group=row_group,
+                  packed=packed)
     _check(_cascade_noalloc(ctypes.byref(a), _stream(stream)), "d2sd_cascade_verify_attention_noalloc")
     return out, lse
 

@@ -47,7 +47,7 @@ class Case:
                                  poison_slack=poison_slack) if tensors else None
 
     # ---- HIP path ----
-    def attention(self, stage=0, kv_split=0, out=None, lse=None, host_offsets=False, row_group=0):
+    def attention(self, stage=0, kv_split=0, out=None, lse=None, host_offsets=False, row_group=0, packed=0):
         """host_offsets: hand the host copy of the node offsets to the planner,
         as the benchmark does (the automatic split then counts work items exactly)."""
         m = d2sd()
@@ -56,17 +56,25 @@ class Case:
             x["q"], x["k_cache"], x["v_cache"], self.d_pt, self.d_ctx, x["k_tree"], x["v_tree"], self.d_ip,
             self.tree["anc_mask"], total_nodes=self.total, max_nodes=self.max_nodes,
             max_ctx_len=int(self.layout.ctx_len.max(initial=0)), stage=stage, kv_split=kv_split, out=out,
-            lse=lse, node_indptr_host=self.node_indptr if host_offsets else None, row_group=row_group)
+            lse=lse, node_indptr_host=self.node_indptr if host_offsets else None, row_group=row_group,
+            packed=packed)
 
-    def resolved_split(self, kv_split=0, host_offsets=False):
-        """The split length the library takes for this batch."""
+    def _args(self, kv_split=0, host_offsets=False, row_group=0, packed=0, stage=0):
         m = d2sd()
         x = self.x
-        a = m.attn_args(x["q"], x["k_cache"], x["v_cache"], self.d_pt, self.d_ctx, x["k_tree"], x["v_tree"],
-                        self.d_ip, self.tree["anc_mask"], x["q"], None, total_nodes=self.total,
-                        max_nodes=self.max_nodes, max_ctx_len=int(self.layout.ctx_len.max(initial=0)),
-                        kv_split=kv_split, node_indptr_host=self.node_indptr if host_offsets else None)
-        return m.cascade_kv_split(a)
+        return m.attn_args(x["q"], x["k_cache"], x["v_cache"], self.d_pt, self.d_ctx, x["k_tree"], x["v_tree"],
+                           self.d_ip, self.tree["anc_mask"], x["q"], None, total_nodes=self.total,
+                           max_nodes=self.max_nodes, max_ctx_len=int(self.layout.ctx_len.max(initial=0)),
+                           kv_split=kv_split, node_indptr_host=self.node_indptr if host_offsets else None,
+                           row_group=row_group, packed=packed, stage=stage)
+
+    def resolved_split(self, kv_split=0, host_offsets=False, **kw):
+        """The split length the library takes for this batch."""
+        return d2sd().cascade_kv_split(self._args(kv_split, host_offsets, **kw))
+
+    def shape(self, kv_split=0, host_offsets=False, **kw):
+        """(rows per workgroup, packed) the library takes for this batch."""
+        return d2sd().cascade_shape(self._args(kv_split, host_offsets, **kw))
 
     def noncascade(self):
         m = d2sd()

@@ -285,17 +285,30 @@ def _best_splits(g, R, s_lo, s_hi):
     return best_s, best
 
 
-def _documented_plan(g4, g12, ctx, min_split=256, gain=1.08):
-    """(split, rows per workgroup) the planner documents for grids that fill
-    the chip with one split: each shape's best split count, and the shape
-    with the shorter time, the 384-row shape counted 8% faster."""
+def _documented_plan(g4, g12, tiles1, ctx, min_split=256, gain=1.08):
+    """(split, rows per workgroup, packed) the planner documents for grids that
+    fill the chip with one split: each shape's best split count, and the shape
+    with the shorter time, the 384-row shapes counted 8% faster; the packed
+    shape (tiles1 query tiles per split, twelve per workgroup, splits of at
+    most 16384 tokens) when it is at least as fast as the one-stream one."""
     s_lo = max(1, -(-ctx // 32768))
     s_hi = max(s_lo, ctx // min_split)
     s4, t4 = _best_splits(g4, 768, s_lo, s_hi)
     s12, t12 = _best_splits(g12, 256, s_lo, s_hi)
-    s, rows = (s12, 384) if t12 / gain < t4 else (s4, 128)
+    s_lo_p = max(s_lo, -(-ctx // 16384))
+    ptime = lambda s: -(-(-(-tiles1 * s // 12)) // 256) / s
+    sp, tp = s_lo_p, ptime(s_lo_p)
+    for s in range(s_lo_p + 1, min(s_hi, 4 * s_lo_p) + 1):
+        if ptime(s) < 0.97 * tp:
+            sp, tp = s, ptime(s)
+    if tiles1 and tp / gain < 0.97 * t12 / gain and tp / gain < t4:
+        s, rows, packed = sp, 384, True
+    elif t12 / gain < t4:
+        s, rows, packed = s12, 384, False
+    else:
+        s, rows, packed = s4, 128, False
     per = -(-ctx // s)
-    return -(-per // 64) * 64, rows
+    return -(-per // 64) * 64, rows, packed
 
 
 @pytest.mark.parametrize("cfg", [4, 5])
@@ -309,17 +322,23 @@ def test_automatic_split_counts_rounds(cfg):
     G = lay.spec.hq // lay.spec.hkv
     g4 = int((-(-(n * G) // 128)).sum()) * lay.spec.hkv
     g12 = int((-(-(n * G) // 384)).sum()) * lay.spec.hkv
+    t = -(-(n * G) // 32)
+    tiles1 = int(t.sum()) * lay.spec.hkv if t.min() >= 6 else 0
     ctx = int(lay.ctx_len.max())
     a = good_args(batch=lay.batch, num_qo_heads=lay.spec.hq, num_kv_heads=lay.spec.hkv, total_nodes=int(ip[-1]),
                   max_nodes=int(n.max()), max_ctx_len=ctx, num_pages=lay.num_pages, max_pages=lay.max_pages,
                   mask_words=W)
     _with_host_indptr(a, ip)
-    split, rows = d2sd.cascade_kv_split(a), d2sd.cascade_row_group(a)
-    assert (split, rows) == _documented_plan(g4, g12, ctx)
-    # 32 requests: 768 four-wave groups (one round) or 256 twelve-wave groups (one round, each context
-    # read once) -> 384 rows, one split; 64 requests with 64 query heads: 2800 four-wave groups, three
-    # splits (10.9 rounds), against 12-wave groups that leave a sixth of their waves idle -> 128 rows
-    assert (g4, -(-ctx // split), rows) == {4: (768, 1, 384), 5: (2800, 3, 128)}[cfg]
+    split = d2sd.cascade_kv_split(a)
+    rows, packed = d2sd.cascade_shape(a)
+    assert (split, rows, packed) == _documented_plan(g4, g12, tiles1, ctx)
+    # 32 requests: 768 four-wave groups (one round), 256 one-stream twelve-wave groups (one round, each
+    # context read once) or 224 packed workgroups (also one round: no gain) -> one-stream 384-row
+    # workgroups, one split; 64 requests with 64 query heads: 2800 four-wave groups (three splits: 10.9
+    # rounds) against 1740 packed workgroups at two splits (6.8 rounds of 256) -> packed, two splits
+    assert (g4, -(-ctx // split), rows, packed) == {4: (768, 1, 384, False), 5: (2800, 2, 384, True)}[cfg]
+    a.packed = 1                                     # one stream per workgroup: the plans without packing
+    assert (d2sd.cascade_kv_split(a), *d2sd.cascade_shape(a)) == _documented_plan(g4, g12, 0, ctx)
 
 
 def test_row_group_is_validated_and_can_be_forced():
@@ -331,6 +350,15 @@ def test_row_group_is_validated_and_can_be_forced():
     assert d2sd.cascade_row_group(good_args(row_group=384, **small)) == 384
     assert d2sd.cascade_row_group(good_args(row_group=128)) == 128
     assert d2sd.cascade_row_group(good_args(row_group=384, dtype=d2sd.F32, **small)) == 128   # fp32: one shape
+    for bad in (-1, 3):
+        assert ws_size(good_args(packed=bad))[0] == d2sd.ERR_INVALID_ARG and "packed" in d2sd.last_error()
+    # packed needs the host node offsets and >= 6 tiles per stream; otherwise one stream per workgroup
+    assert d2sd.cascade_shape(good_args(row_group=384, packed=2)) == (384, False)
+    ip = np.arange(33, dtype=np.int32) * 80                              # 80 nodes x 4 heads = 10 tiles
+    assert d2sd.cascade_shape(_with_host_indptr(good_args(row_group=384, packed=2), ip)) == (384, True)
+    ip = np.concatenate([[0], np.cumsum([80] * 31 + [40])]).astype(np.int32)   # one request of 5 tiles
+    assert d2sd.cascade_shape(_with_host_indptr(good_args(row_group=384, packed=2, total_nodes=int(ip[-1])),
+                                                ip)) == (384, False)
 
 
 def test_workspace_sizing_and_too_small():

@@ -17,9 +17,10 @@ pytestmark = pytest.mark.gpu
 ROW_GROUPS = [0, 384]
 
 
-def check_full(case, stage="cascade", kv_split=0, out=None, lse=None, row_group=0):
+def check_full(case, stage="cascade", kv_split=0, out=None, lse=None, row_group=0, packed=0, host_offsets=False):
     code = {"cascade": 0, "prefix": 1, "tree": 2}[stage]
-    o, l = case.attention(stage=code, kv_split=kv_split, row_group=row_group)
+    o, l = case.attention(stage=code, kv_split=kv_split, row_group=row_group, packed=packed,
+                          host_offsets=host_offsets)
     torch.cuda.synchronize()
     o = o.double().cpu().numpy()
     l = l.cpu().numpy()
@@ -250,3 +251,47 @@ def test_full_size_sampled(cfg):
         assert max(max_abs(og, ow), max_abs(lg, lw)) <= tol, (cfg, b)
     # properties that hold everywhere: finite outputs, |o| bounded by max |v|
     assert torch.isfinite(o.float()).all() and torch.isfinite(l).all()
+
+
+# ---- the packed twelve-wave kernel (workgroups over the sequence of all streams' query tiles) ----
+
+def check_packed(lay, kv_split=0, stages=("cascade",), poison=True):
+    case = Case(lay, poison_slack=poison)
+    for stage in stages:
+        code = {"cascade": 0, "prefix": 1, "tree": 2}[stage]
+        assert case.shape(kv_split, host_offsets=True, row_group=384, packed=2, stage=code) == (384, True)
+        check_full(case, stage, kv_split, row_group=384, packed=2, host_offsets=True)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_packed_random_layouts(seed):
+    """Random batches with 32 query heads per KV head (a node is a whole
+    tile, so every stream holds >= B >= 8 tiles), ragged and empty contexts,
+    poisoned page slack, contexts past one split, several split lengths;
+    every row against the oracle."""
+    rng = np.random.default_rng(3000 + seed)
+    batch = int(rng.integers(1, 9))
+    B = int(rng.choice([8, 16, 24]))
+    rows = [sorted(rng.choice(np.arange(1, B), int(rng.integers(0, B)), replace=False).tolist())
+            for _ in range(batch)]
+    ctx = [int(c) for c in rng.choice([0, 1, 15, 17, 33, 100, 1000, 3000, 17000, 40000], batch)]
+    kv_split = int(rng.choice([0, 64, 256, 1024, 16384])) if max(ctx) <= 3000 else int(rng.choice([0, 16384]))
+    lay = wl.custom_layout(B, rows, ctx, hq=64, hkv=2, dtype="bf16", seed=seed)
+    check_packed(lay, kv_split)
+
+
+def test_packed_three_streams_per_workgroup():
+    """Exactly six tiles per stream (48 nodes x 4 query heads per KV head):
+    twelve consecutive tiles span two or three streams."""
+    p = [2, 5, 11, 14]                                  # 16 + 14 + 11 + 5 + 2 = 48 nodes: 192 rows, 6 tiles
+    lay = wl.custom_layout(16, [p] * 7, [700, 31, 0, 2000, 64, 333, 1500], hq=8, hkv=2, dtype="bf16", seed=31)
+    check_packed(lay, 0, stages=("cascade", "prefix", "tree"))
+    check_packed(lay, 256)
+
+
+@pytest.mark.parametrize("kv_split", [0, 1024])
+def test_packed_stages_and_tree_tiles(kv_split):
+    """Large trees (B = 32, up to 4 tree tiles after the context) in every stage."""
+    lay = wl.custom_layout(32, [[1, 5, 9, 20, 31], [], [3, 4, 5, 6, 7, 8], [30]], [4000, 0, 77, 1025], hq=32, hkv=4,
+                           dtype="bf16", seed=32)
+    check_packed(lay, kv_split, stages=("cascade", "prefix", "tree"))

@@ -6,8 +6,8 @@ host copy of the node offsets):
     row and lse of every request (83,488 rows);
   * 64 requests x 32768-token contexts, 64 query / 8 KV heads: every row of
     16 whole requests, the smallest and the largest tree among them, taken
-    from the launch over the whole batch (three context splits, so the
-    split merge runs at full size).
+    from the launch over the whole batch (two or more context splits, so
+    the split merge runs at full size).
 
 Each request's rows are compared with the float64 oracle (the definition:
 one softmax over the whole context and the node's ancestors-or-self), max
@@ -66,13 +66,15 @@ def check_requests(cfg, reqs):
 def test_ctx16k_b32_every_row(part):
     case, _, _ = full_run(4)
     assert case.resolved_split(host_offsets=True) == 16384       # one split, as the benchmark runs it
+    print("shape (rows per workgroup, packed):", case.shape(host_offsets=True), flush=True)
     check_requests(4, range(8 * part, 8 * part + 8))
 
 
 @pytest.mark.parametrize("part", range(4))
 def test_ctx32k_b64_whole_requests(part):
     case, _, _ = full_run(5)
-    assert -(-32768 // case.resolved_split(host_offsets=True)) == 3   # three splits and the merge
+    assert -(-32768 // case.resolved_split(host_offsets=True)) >= 2   # the split merge runs
+    print("shape (rows per workgroup, packed):", case.shape(host_offsets=True), flush=True)
     reqs = cfg5_requests()
     n = np.diff(case.node_indptr)
     assert len(set(reqs)) == 16 and n[reqs[0]] == n.min() and n[reqs[1]] == n.max()
