@@ -81,6 +81,10 @@ def parse():
                          "(measured no faster than eager launches: the step is not launch-bound)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy three times (HBM counter calibration)")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="host only: average duration of the attention kernel and the split merge per bench phase "
+                         "(warm-up, cold, warm, back to back; --warmup/--steps of the traced run) from a rocprofv3 "
+                         "kernel trace under DIR")
     ap.add_argument("--record-traffic", metavar="DIR",
                     help="host only: derive the attention kernel's HBM bytes per launch from rocprofv3 counter "
                          "CSVs under DIR (fetch/, write/, copy_fetch/, copy_write/, and fetch.log holding the "
@@ -159,6 +163,51 @@ def _counter_per_dispatch(csv_dir: str, kernel: str, counter: str) -> float:
     return sum(per.values()) / len(per)
 
 
+def trace_summary(d: str, warmup: int, steps: int) -> dict:
+    """Mean duration (us) of every attention kernel and split merge in a
+    rocprofv3 kernel trace, per phase of a default bench run: `warmup`
+    warm-up steps, then `steps` cold, `steps` warm and `steps` back-to-back
+    steps, each with one attention call (dispatches in start order)."""
+    import csv
+    import glob
+
+    paths = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    if not paths:
+        raise FileNotFoundError(f"no kernel_trace.csv under {d}")
+    names = ["cascade_bf16_packed_kernel", "cascade_bf16_wide_kernel", "cascade_bf16_kernel",
+             "cascade_attention_kernel", "split_merge_kernel"]
+    per = {}
+    for path in paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                for k in names:
+                    if kernel_name_matches(r["Kernel_Name"], k):
+                        per.setdefault(k, []).append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    bounds = {"warmup": (0, warmup), "cold": (warmup, warmup + steps),
+              "warm": (warmup + steps, warmup + 2 * steps), "backtoback": (warmup + 2 * steps, warmup + 3 * steps)}
+    out = {}
+    for k, ev in per.items():
+        dur = [(e - s_) / 1e3 for s_, e in sorted(ev)]
+        out[k] = {"dispatches": len(dur), "all": round(float(np.mean(dur)), 1)}
+        for ph, (a, b) in bounds.items():
+            if len(dur) >= b:
+                out[k][ph] = round(float(np.mean(dur[a:b])), 1)
+    return out
+
+
+def attention_kernel_name(line: dict) -> str:
+    """The attention kernel a bench line's launch ran: by dtype and
+    workgroup shape (config.row_group, config.packed)."""
+    if line.get("dtype") != "bf16":
+        return "cascade_attention_kernel"
+    cfg = line.get("config", {})
+    if cfg.get("packed"):
+        return "cascade_bf16_packed_kernel"
+    if cfg.get("row_group") == 384:
+        return "cascade_bf16_wide_kernel"
+    return "cascade_bf16_kernel"
+
+
 def record_traffic(d: str):
     """Write the attention kernel's measured HBM bytes per launch. FETCH_SIZE and
     WRITE_SIZE (KiB per dispatch) are scaled by what they read for a 1 GiB
@@ -166,7 +215,7 @@ def record_traffic(d: str):
     with open(os.path.join(d, "fetch.log")) as f:
         line = [ln for ln in f.read().splitlines() if ln.startswith("{")][-1]
     bench = json.loads(line)
-    kern = "cascade_bf16_kernel" if bench["dtype"] == "bf16" else "cascade_attention_kernel"
+    kern = attention_kernel_name(bench)
     fetch = _counter_per_dispatch(os.path.join(d, "fetch"), kern, "FETCH_SIZE")
     write = _counter_per_dispatch(os.path.join(d, "write"), kern, "WRITE_SIZE")
     if bench.get("roofline", {}).get("splits", 1) > 1:
@@ -184,7 +233,7 @@ def record_traffic(d: str):
             rec = json.load(f)
     rec[f"config{cfg_num}"] = {
         "workload": cfg["workload"], "kernel_sha": kernel_sha(), "kv_split": bench.get("requested_kv_split", 0),
-        "resolved_kv_split": cfg["kv_split"], "fetch_kib_per_dispatch": round(fetch, 1),
+        "resolved_kv_split": cfg["kv_split"], "kernel": kern, "fetch_kib_per_dispatch": round(fetch, 1),
         "write_kib_per_dispatch": round(write, 1), "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4),
         "hbm_bytes_per_launch": int(round((fetch * f_fac + write * w_fac) * 1024)),
         "summary": f"profiles/cascade_attention_{cfg['workload']}.md",
@@ -318,6 +367,9 @@ def main():
         return
     if args.record_traffic:
         record_traffic(args.record_traffic)
+        return
+    if args.trace_summary:
+        print(json.dumps(trace_summary(args.trace_summary, args.warmup, args.steps)), flush=True)
         return
 
     import torch

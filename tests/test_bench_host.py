@@ -95,6 +95,32 @@ def test_record_traffic_adds_the_split_merge(tmp_path, monkeypatch):
     assert r["hbm_bytes_per_launch"] == (1300 + 140) * 1024
 
 
+def test_trace_summary_phases(tmp_path):
+    d = tmp_path / "kt"
+    os.makedirs(d)
+    with open(d / "run_kernel_trace.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        t = 0
+        for i in range(2 + 3 * 4):              # warmup 2, steps 4: 14 attention calls, durations 1..14 us
+            w.writerow({"Kernel_Name": "ns::cascade_bf16_wide_kernel(P)", "Start_Timestamp": t,
+                        "End_Timestamp": t + 1000 * (i + 1)})
+            w.writerow({"Kernel_Name": "ns::noncascade_bf16_kernel(P)", "Start_Timestamp": t + 1,
+                        "End_Timestamp": t + 99999})
+            t += 100000
+    r = bench.trace_summary(str(d), 2, 4)["cascade_bf16_wide_kernel"]
+    assert r == {"dispatches": 14, "all": 7.5, "warmup": 1.5, "cold": 4.5, "warm": 8.5, "backtoback": 12.5}
+    assert "noncascade_bf16_kernel" not in bench.trace_summary(str(d), 2, 4)
+
+
+def test_attention_kernel_name_follows_the_shape():
+    k = bench.attention_kernel_name
+    assert k({"dtype": "f32", "config": {}}) == "cascade_attention_kernel"
+    assert k({"dtype": "bf16", "config": {"row_group": 128}}) == "cascade_bf16_kernel"
+    assert k({"dtype": "bf16", "config": {"row_group": 384, "packed": False}}) == "cascade_bf16_wide_kernel"
+    assert k({"dtype": "bf16", "config": {"row_group": 384, "packed": True}}) == "cascade_bf16_packed_kernel"
+
+
 def test_kernel_names_match_whole_identifiers():
     m = bench.kernel_name_matches
     assert m("d2sd::(anonymous namespace)::cascade_bf16_kernel(d2sd::(anonymous namespace)::Params)",
