@@ -377,7 +377,9 @@ d2sd_status make_plan(const d2sd_attn_args* a, d2sd::AttnPlan* plan) {
     return fail(D2SD_ERR_UNSUPPORTED, "too many split-merge workgroups (batch %d, max_nodes %d)", a->batch,
                 a->max_nodes);
   const size_t rows = (size_t)a->total_nodes * a->num_qo_heads;
-  plan->ws_bytes = plan->n_ch_max > 1 ? (size_t)plan->n_ch_max * rows * (a->head_dim + 2) * sizeof(float) : 0;
+  // per split and row: the normalised output in the input dtype, then m and l in fp32
+  const size_t o_elem = a->dtype == D2SD_BF16 ? 2 : 4;
+  plan->ws_bytes = plan->n_ch_max > 1 ? (size_t)plan->n_ch_max * rows * (a->head_dim * o_elem + 2 * sizeof(float)) : 0;
   plan->scale = a->sm_scale > 0.0f ? a->sm_scale : 1.0f / sqrtf((float)a->head_dim);
   return D2SD_OK;
 }

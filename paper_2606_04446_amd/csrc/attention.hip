@@ -55,7 +55,7 @@ struct Params {
   const uint32_t* anc_mask;
   void* out;
   float* lse;
-  float* ws_o;  // [n_ch_max, total_rows, D]
+  void* ws_o;   // [n_ch_max, total_rows, D] split outputs normalised by their row sum, in the input dtype
   float* ws_m;  // [n_ch_max, total_rows]
   float* ws_l;  // [n_ch_max, total_rows]
   int batch, hq, hkv, G, stage;
@@ -410,15 +410,16 @@ __device__ __forceinline__ void attention_body(const Params& p) {
         p.lse[row] = l_all > 0.0f ? (m_run[j] * p.c2 + __log2f(l_all)) * kLn2 : -INFINITY;
     } else {
       const size_t prow = (size_t)ch * ((size_t)p.total_nodes * p.hq) + row;
-      float* dst = p.ws_o + prow * kD;
+      const float inv = l_all > 0.0f ? 1.0f / l_all : 0.0f;
+      T* dst = static_cast<T*>(p.ws_o) + prow * kD;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           float v[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = o[j][dt][q4 * 4 + r];
-          store_out<float>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+          for (int r = 0; r < 4; ++r) v[r] = o[j][dt][q4 * 4 + r] * inv;
+          store_out<T>(dst + dt * 32 + q4 * 8 + hf * 4, v);
         }
       }
       if (hf == 0) {
@@ -908,15 +909,16 @@ __device__ __forceinline__ void bf16_attention_body(const Params& p) {
     if (p.lse && hf == 0) p.lse[row] = l_all > 0.0f ? (m_run * p.c2 + __log2f(l_all)) * kLn2 : -INFINITY;
   } else {
     const size_t prow = (size_t)ch * ((size_t)p.total_nodes * p.hq) + row;
-    float* dst = p.ws_o + prow * kD;
+    const float inv = l_all > 0.0f ? 1.0f / l_all : 0.0f;
+    __bf16* dst = static_cast<__bf16*>(p.ws_o) + prow * kD;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         float v[4];
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr];
-        store_out<float>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr] * inv;
+        store_out<__bf16>(dst + dt * 32 + q4 * 8 + hf * 4, v);
       }
     }
     if (hf == 0) {
@@ -1271,15 +1273,16 @@ __device__ void bf16_packed_body(const Params& p) {
     if (p.lse && hf == 0) p.lse[row] = l_all > 0.0f ? (m_run * p.c2 + __log2f(l_all)) * kLn2 : -INFINITY;
   } else {
     const size_t prow2 = (size_t)my.ch * ((size_t)p.total_nodes * p.hq) + row;
-    float* dst = p.ws_o + prow2 * kD;
+    const float inv = l_all > 0.0f ? 1.0f / l_all : 0.0f;
+    __bf16* dst = static_cast<__bf16*>(p.ws_o) + prow2 * kD;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         float v[4];
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr];
-        store_out<float>(dst + dt * 32 + q4 * 8 + hf * 4, v);
+        for (int rr = 0; rr < 4; ++rr) v[rr] = o[dt][q4 * 4 + rr] * inv;
+        store_out<__bf16>(dst + dt * 32 + q4 * 8 + hf * 4, v);
       }
     }
     if (hf == 0) {
@@ -1325,6 +1328,22 @@ struct MergeState {
   float acc[8];
 };
 
+// Eight consecutive dims of a split's normalised output.
+__device__ __forceinline__ void load_partial8(const float* src, float (&v)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(src);
+  const float4 b = *reinterpret_cast<const float4*>(src + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void load_partial8(const __bf16* src, float (&v)[8]) {
+  const uint4 u = *reinterpret_cast<const uint4*>(src);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
 template <typename T, int GROUPS>
 __global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p, int chunks) {
   constexpr int ROWS = merge_rows(GROUPS);
@@ -1351,14 +1370,13 @@ __global__ __launch_bounds__(kThreads) void split_merge_kernel(Params p, int chu
       const size_t pr = s * stride + row;
       const float ms = p.ws_m[pr];
       const float ls = p.ws_l[pr];
-      const float4 v0 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0);
-      const float4 v1 = *reinterpret_cast<const float4*>(p.ws_o + pr * kD + d0 + 4);
+      float v[8];
+      load_partial8(static_cast<const T*>(p.ws_o) + pr * kD + d0, v);
       const float Mn = fmaxf(M, ms);
       if (Mn == -INFINITY) continue;                        // no keys so far
       const float a = __builtin_amdgcn_exp2f(M - Mn);       // 0 while M is -inf
-      const float w = __builtin_amdgcn_exp2f(ms - Mn);      // 0 for an empty split
-      const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-      L = L * a + w * ls;
+      const float w = __builtin_amdgcn_exp2f(ms - Mn) * ls; // 0 for an empty split
+      L = L * a + w;
 #pragma unroll
       for (int i = 0; i < 8; ++i) acc[i] = acc[i] * a + w * v[i];
       M = Mn;
@@ -1428,9 +1446,11 @@ Params make_params(const d2sd_attn_args& a, const AttnPlan& plan, void* ws) {
   p.ctx_len = a.ctx_len; p.k_tree = a.k_tree; p.v_tree = a.v_tree; p.node_indptr = a.node_indptr;
   p.anc_mask = a.anc_mask; p.out = a.out; p.lse = a.lse;
   const size_t rows = (size_t)a.total_nodes * a.num_qo_heads;
-  float* w = static_cast<float*>(ws);
+  // [normalised O in the input dtype][m][l] (fp32), each split-major
+  char* w = static_cast<char*>(ws);
+  const size_t o_bytes = (size_t)plan.n_ch_max * rows * kD * (a.dtype == D2SD_BF16 ? 2 : 4);
   p.ws_o = w;
-  p.ws_m = w ? w + (size_t)plan.n_ch_max * rows * kD : nullptr;
+  p.ws_m = w ? reinterpret_cast<float*>(w + o_bytes) : nullptr;
   p.ws_l = w ? p.ws_m + (size_t)plan.n_ch_max * rows : nullptr;
   p.batch = a.batch; p.hq = a.num_qo_heads; p.hkv = a.num_kv_heads; p.G = plan.G; p.stage = a.stage;
   p.total_nodes = a.total_nodes; p.max_nodes = a.max_nodes; p.max_ctx = a.max_ctx_len;

@@ -366,7 +366,9 @@ def test_workspace_sizing_and_too_small():
     st, n = ws_size(a)
     assert st == 0
     rows = a.total_nodes * a.num_qo_heads
-    assert n == 4 * rows * (128 + 2) * 4          # 4 splits of fp32 partial states
+    assert n == 4 * rows * (128 * 2 + 2 * 4)      # 4 splits: bf16 normalised outputs, fp32 m and l
+    a32 = good_args(kv_split=4096, dtype=d2sd.F32)
+    assert ws_size(a32) == (0, 4 * rows * (128 * 4 + 2 * 4))   # fp32 inputs keep fp32 partial outputs
     assert d2sd._cascade(ctypes.byref(a), ctypes.c_void_p(FAKE), n - 1, None) == d2sd.ERR_WORKSPACE_TOO_SMALL
     assert "need" in d2sd.last_error()
     a = good_args(kv_split=16384)                  # one split: finalised in place

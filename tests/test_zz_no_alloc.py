@@ -15,14 +15,17 @@ pytestmark = pytest.mark.gpu
 SCRATCH_BYTES = 64 << 20
 
 
-def call_both(case, kv_split=0):
-    """(noalloc out, lse), (workspace out, lse), workspace bytes of the plan."""
+def call_both(case, kv_split=0, host_offsets=False):
+    """(noalloc out, lse), (workspace out, lse), workspace bytes of the plan.
+    host_offsets: both calls plan from the host copy of the node offsets, as
+    the benchmark does."""
     m = d2sd()
     x = case.x
     ins = (x["q"], x["k_cache"], x["v_cache"], case.d_pt, case.d_ctx, x["k_tree"], x["v_tree"], case.d_ip,
            case.tree["anc_mask"])
     kw = dict(total_nodes=case.total, max_nodes=case.max_nodes,
-              max_ctx_len=int(case.layout.ctx_len.max(initial=0)), kv_split=kv_split)
+              max_ctx_len=int(case.layout.ctx_len.max(initial=0)), kv_split=kv_split,
+              node_indptr_host=case.node_indptr if host_offsets else None)
     ws = m.cascade_workspace_size(m.attn_args(*ins, x["q"], None, **kw))
     o_ref, l_ref = m.cascade_verify_attention(*ins, **kw)
     o = torch.full_like(x["q"], float("nan"))
@@ -49,18 +52,21 @@ def test_two_calls_in_a_row_second_smaller():
 
 
 def test_automatic_plan_larger_than_the_scratch():
-    """The 8-request batch's automatic plan (twelve splits of 704 tokens, 77 MB
-    of partial states) does not fit: the entry point takes fewer, longer
-    splits; the result matches the workspace entry point within the bf16
-    tolerance and the oracle on every row."""
-    case = Case(wl.draw_layout(3))
-    (o, l), (o_ref, l_ref), ws = call_both(case)
+    """The 64-request, 32k-context batch's automatic plan from the host node
+    offsets (the packed shape, two splits of 16384 tokens, 173 MB of partial
+    states) does not fit: the entry point takes fewer, longer splits (here one,
+    which needs none). Every row matches the workspace entry point within the
+    bf16 tolerance, and the requests with the smallest and the largest tree
+    match the oracle."""
+    case = Case(wl.draw_layout(5))
+    (o, l), (o_ref, l_ref), ws = call_both(case, host_offsets=True)
     assert ws > SCRATCH_BYTES
     tol = TOL[case.dtype]
     assert max_abs(o.double().cpu().numpy(), o_ref.double().cpu().numpy()) <= tol
     assert max_abs(l.cpu().numpy(), l_ref.cpu().numpy()) <= tol
     o_h, l_h = o.double().cpu().numpy(), l.cpu().numpy()
-    for b in range(case.layout.batch):
+    sizes = np.diff(case.node_indptr)
+    for b in sorted({int(np.argmin(sizes)), int(np.argmax(sizes))}):
         s, e = int(case.node_indptr[b]), int(case.node_indptr[b + 1])
         ow, lw = case.oracle_attention(b)
         assert max(max_abs(o_h[s:e], ow), max_abs(l_h[s:e], lw)) <= tol, b
