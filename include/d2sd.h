@@ -8,9 +8,10 @@
  *   d2sd_tree_build       device  canonical tree arrays + ancestor-or-self masks
  *   d2sd_cascade_verify_attention
  *                         device  shared-prefix (context) attention, each context
- *                                 slab read once per (split, 128-row group) and
- *                                 shared by the tree nodes and GQA heads of the
- *                                 group, plus tree-suffix attention under the
+ *                                 slab read once per (split, workgroup of up to
+ *                                 384 query rows) and shared by the tree nodes
+ *                                 and GQA heads it holds, plus tree-suffix
+ *                                 attention under the
  *                                 ancestor mask, states merged by log-sum-exp
  *   d2sd_merge_state      device  the log-sum-exp merge of two attention states
  *   d2sd_accept_path      device  greedy longest-accepted-path selection + bonus
@@ -298,11 +299,13 @@ d2sd_status d2sd_cascade_row_group(const d2sd_attn_args* args, int* rows, int* p
 /*
  * Device. Verify attention (see d2sd_attn_args). The M = N_b * G query rows
  * of a (request, KV head) are cut into row groups of 128 or 384 (bf16,
- * d2sd_cascade_row_group); every context page slab is streamed once per
- * (context split, row group) and reused by all rows of the group, i.e. by
- * all G query heads of the group's tree nodes. The row groups of one split
- * run as neighbouring workgroups on one XCD, so that later readers of a slab
- * mostly hit its L2.
+ * d2sd_cascade_row_group), or, in the packed shape, into the 32-row tiles of
+ * the sequence of all (request, KV head, split) streams, twelve consecutive
+ * tiles per workgroup; every context page slab is streamed once per
+ * (context split, workgroup) and reused by all rows the workgroup holds of
+ * that stream, i.e. by all G query heads of their tree nodes. The
+ * workgroups of one stream run as neighbours on one XCD, so that later
+ * readers of a slab can hit its L2.
  * ws: device workspace of ws_bytes >= d2sd_cascade_workspace_size(args) (may
  * be NULL when that size is 0). Concurrent calls must not share a workspace.
  */
