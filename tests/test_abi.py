@@ -359,6 +359,13 @@ def test_row_group_is_validated_and_can_be_forced():
     ip = np.concatenate([[0], np.cumsum([80] * 31 + [40])]).astype(np.int32)   # one request of 5 tiles
     assert d2sd.cascade_shape(_with_host_indptr(good_args(row_group=384, packed=2, total_nodes=int(ip[-1])),
                                                 ip)) == (384, False)
+    # the packed kernel stages the tile counts of at most 2048 requests in LDS
+    for batch, packed in ((2048, True), (2049, False)):
+        ip = np.arange(batch + 1, dtype=np.int32) * 8                      # 8 nodes x 32 heads = 8 tiles
+        a = good_args(row_group=384, packed=2, batch=batch, num_qo_heads=64, num_kv_heads=2,
+                      total_nodes=8 * batch, max_nodes=8, max_ctx_len=64, num_pages=4 * batch, max_pages=4,
+                      mask_words=1)
+        assert d2sd.cascade_shape(_with_host_indptr(a, ip)) == (384, packed), batch
 
 
 def test_workspace_sizing_and_too_small():

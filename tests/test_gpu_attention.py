@@ -289,6 +289,19 @@ def test_packed_three_streams_per_workgroup():
     check_packed(lay, 256)
 
 
+def test_packed_largest_batch():
+    """The largest batch the packed kernel takes (2048 requests: the block
+    scan of the requests' tile counts holds three requests per thread, and the
+    binary search over them runs its full depth), small ragged contexts and
+    one- to four-node branches; every row against the oracle."""
+    rng = np.random.default_rng(2048)
+    rows = [sorted(rng.choice(np.arange(1, 8), int(rng.integers(0, 3)), replace=False).tolist())
+            for _ in range(2048)]
+    ctx = [int(c) for c in rng.choice([0, 1, 16, 17, 40, 64, 100], 2048)]
+    lay = wl.custom_layout(8, rows, ctx, hq=64, hkv=2, dtype="bf16", seed=2048)
+    check_packed(lay, 0, stages=("cascade", "prefix"))
+
+
 @pytest.mark.parametrize("kv_split", [0, 1024])
 def test_packed_stages_and_tree_tiles(kv_split):
     """Large trees (B = 32, up to 4 tree tiles after the context) in every stage."""
