@@ -1,5 +1,5 @@
 """A verify step (tree build, cascade attention, accept path) captured in a
-HIP graph: several replays, with eager work and synchronisations between
+HIP graph, in each attention workgroup shape: several replays, with eager work and synchronisations between
 them, each checked against the eager result; a replay after an in-place
 change of the inputs must see the new values."""
 
@@ -18,10 +18,30 @@ def d2sd():
     return m
 
 
-@pytest.mark.parametrize("cfg", [2, 3])
+def _layout(name):
+    """(layout, attention launch options, expected (rows per workgroup, packed))."""
+    if name in (2, 3):
+        return wl.draw_layout(name), {}, (128, False)
+    rng = np.random.default_rng(77)
+    rows = [sorted(rng.choice(np.arange(1, 16), int(rng.integers(0, 6)), replace=False).tolist()) for _ in range(6)]
+    ctx = [3000, 5000, 17, 2048, 4500, 0]
+    if name == "wide":      # one stream per 384-row workgroup, several splits (the merge is captured too)
+        lay = wl.custom_layout(16, rows, ctx, hq=32, hkv=8, dtype="bf16", seed=78)
+        return lay, dict(kv_split=1024, row_group=384, packed=1), (384, False)
+    # workgroups over the sequence of all streams' tiles, planned from the host node offsets
+    lay = wl.custom_layout(16, rows, ctx, hq=64, hkv=2, dtype="bf16", seed=79)
+    return lay, dict(kv_split=1024, row_group=384, packed=2, host=True), (384, True)
+
+
+@pytest.mark.parametrize("cfg", [2, 3, "wide", "packed"])
 def test_graph_replays_match_eager(cfg):
     m = d2sd()
-    case = Case(wl.draw_layout(cfg))
+    lay, opt, want_shape = _layout(cfg)
+    case = Case(lay)
+    kw = dict(kv_split=opt.get("kv_split", 0), row_group=opt.get("row_group", 0), packed=opt.get("packed", 0),
+              node_indptr_host=case.node_indptr if opt.get("host") else None)
+    assert case.shape(kw["kv_split"], host_offsets=bool(opt.get("host")), row_group=kw["row_group"],
+                      packed=kw["packed"]) == want_shape
     x = case.x
     B, total, W = case.B, case.total, case.W
     dev = torch.device("cuda")
@@ -33,7 +53,7 @@ def test_graph_replays_match_eager(cfg):
     max_ctx = int(case.layout.ctx_len.max())
     args = m.attn_args(x["q"], x["k_cache"], x["v_cache"], case.d_pt, case.d_ctx, x["k_tree"], x["v_tree"],
                        case.d_ip, tree["anc_mask"], out, lse, total_nodes=total, max_nodes=case.max_nodes,
-                       max_ctx_len=max_ctx)
+                       max_ctx_len=max_ctx, **kw)
     ws = torch.empty(max(m.cascade_workspace_size(args), 1), dtype=torch.uint8, device=dev)
     acc = m.accept_path(B, case.d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax)
 
@@ -41,7 +61,8 @@ def test_graph_replays_match_eager(cfg):
         m.tree_build(B, case.d_K, case.d_p, case.d_ip, total, W, out=tree)
         m.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], case.d_pt, case.d_ctx, x["k_tree"],
                                    x["v_tree"], case.d_ip, tree["anc_mask"], total_nodes=total,
-                                   max_nodes=case.max_nodes, max_ctx_len=max_ctx, out=out, lse=lse, workspace=ws)
+                                   max_nodes=case.max_nodes, max_ctx_len=max_ctx, out=out, lse=lse, workspace=ws,
+                                   **kw)
         m.accept_path(B, case.d_ip, total, tree["parent"], tree["depth"], tree["path_id"], d_draft, d_argmax,
                       out=acc)
 
