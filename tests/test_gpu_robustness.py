@@ -93,6 +93,48 @@ def test_attention_with_inconsistent_offsets_lengths_and_pages(dtype):
     assert torch.equal(again, ref) and torch.equal(again_lse, ref_lse)
 
 
+@pytest.mark.parametrize("shape", ["wide", "packed"])
+def test_twelve_wave_attention_with_inconsistent_device_arrays(shape):
+    """The twelve-wave shapes, planned from valid host node offsets (the packed
+    one maps every wave to its stream from the device offsets), run on garbage
+    device offsets, context lengths and page ids: guards intact, inputs
+    unchanged, a valid call afterwards unchanged."""
+    m = d2sd()
+    lay = wl.custom_layout(16, [[3, 7], [2], [], [5, 9, 12], [1]], [3000, 40, 0, 2570, 700], hq=32, hkv=2,
+                           dtype="bf16", seed=4)
+    c = Case(lay)
+    x = c.x
+    opt = dict(row_group=384, packed=1 if shape == "wide" else 2, node_indptr_host=c.node_indptr)
+    assert c.shape(1024, host_offsets=True, row_group=384, packed=opt["packed"]) == (384, shape == "packed")
+    rng = np.random.default_rng([6, int(shape == "packed")])
+    max_ctx = int(c.layout.ctx_len.max())
+    ref, ref_lse = c.attention(kv_split=1024, host_offsets=True, row_group=384, packed=opt["packed"])
+    torch.cuda.synchronize()
+    inputs = {k: v.clone() for k, v in x.items()}
+    bad_ip = garbage_i32(rng, lay.batch + 1)
+    bad_ctx = garbage_i32(rng, lay.batch)
+    bad_pt = garbage_i32(rng, c.d_pt.numel()).view_as(c.d_pt)
+    for kv_split in (1024, 0):
+        obuf, out = guarded(tuple(x["q"].shape), x["q"].dtype, 7.0)
+        lbuf, lse = guarded(tuple(x["q"].shape[:2]), torch.float32, 7.0)
+        a = m.attn_args(x["q"], x["k_cache"], x["v_cache"], bad_pt, bad_ctx, x["k_tree"], x["v_tree"], bad_ip,
+                        c.tree["anc_mask"], out, lse, total_nodes=c.total, max_nodes=c.max_nodes,
+                        max_ctx_len=max_ctx, kv_split=kv_split, **opt)
+        need = m.cascade_workspace_size(a)
+        wbuf, ws = guarded((max(need, 1),), torch.uint8, 0x5A)
+        m.cascade_verify_attention(x["q"], x["k_cache"], x["v_cache"], bad_pt, bad_ctx, x["k_tree"], x["v_tree"],
+                                   bad_ip, c.tree["anc_mask"], total_nodes=c.total, max_nodes=c.max_nodes,
+                                   max_ctx_len=max_ctx, kv_split=kv_split, out=out, lse=lse, workspace=ws, **opt)
+        torch.cuda.synchronize()
+        assert guard_intact(obuf, out.shape, 7.0) and guard_intact(lbuf, lse.shape, 7.0)
+        assert guard_intact(wbuf, ws.shape, 0x5A)
+    for k, v in inputs.items():
+        assert torch.equal(x[k], v), k
+    again, again_lse = c.attention(kv_split=1024, host_offsets=True, row_group=384, packed=opt["packed"])
+    torch.cuda.synchronize()
+    assert torch.equal(again, ref) and torch.equal(again_lse, ref_lse)
+
+
 def test_tree_kernels_with_inconsistent_inputs():
     m = d2sd()
     rng = np.random.default_rng(6)
