@@ -181,12 +181,18 @@ def test_merge_state_against_oracle():
     assert max_abs(lm.cpu().numpy(), lw) <= 1e-5
 
 
-def test_deterministic():
-    case = Case(wl.draw_layout(3))
-    o1, l1 = case.attention()
-    o2, l2 = case.attention()
+@pytest.mark.parametrize("cfg", [3, 4, 5])
+def test_deterministic(cfg):
+    """Two calls give the same bits, in the launch the benchmark makes (planned
+    from the host node offsets): four-wave groups with twelve splits, one
+    384-row workgroup per request and KV head, and the packed kernel with two
+    splits and the merge."""
+    case = Case(wl.draw_layout(cfg))
+    o1, l1 = case.attention(host_offsets=True)
+    o2, l2 = case.attention(host_offsets=True)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert case.shape(host_offsets=True) == {3: (128, False), 4: (384, False), 5: (384, True)}[cfg]
 
 
 def test_kernel_timing_per_launch():
