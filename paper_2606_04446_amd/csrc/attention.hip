@@ -20,14 +20,18 @@
 // stays lane-local. P^T leaves the accumulator already in MFMA B-operand
 // order, and O^T += V^T P^T takes the V^T fragments in the matching key order
 // (bf16: transposing LDS reads of the row-major V tile; fp32: per-element
-// reads of the key-major tile). Split partials (unnormalised O, running max in
-// log2 units, running sum) go to the workspace and a second kernel merges them
-// by log-sum-exp; a request with a single split is finalised in place.
+// reads of the key-major tile). Split partials (O divided by its row sum, in
+// the input dtype; running max in log2 units and running sum in fp32) go to
+// the workspace and a second kernel merges them by log-sum-exp; a request with
+// a single split is finalised in place.
 //
 // The fp32 kernel stages tiles through registers. The bf16 kernel copies them
-// by LDS DMA, runs three 40 KB workgroups per CU (three independent waves per
-// SIMD), moves the running max (and rescales O and l) only when it grows by
-// more than 2^8, and skips masking on interior context tiles.
+// by LDS DMA, in one of three workgroup shapes (three waves per SIMD in each):
+// 4 waves of 32 query rows, three workgroups per CU; 12 waves sharing one K/V
+// ring, one workgroup per CU; or 12 waves over the sequence of all streams'
+// query tiles (the packed kernel). It moves the running max (and rescales O
+// and l) only when it grows by more than 2^8, and skips masking on interior
+// context tiles.
 #include <math.h>
 
 #include <mutex>
